@@ -1,0 +1,277 @@
+"""Pins for the oracle's plan and permutation (CPU only).
+
+Each test checks the oracle against something other than itself: the worked
+example of Sec. 2.1, hand traces of Alg. 2/3, exhaustive search, closed forms
+and invariants the paper states (Sec. 4: capacity, native-first, the plan
+equals standard EP when the routing is balanced).
+"""
+
+import json
+import math
+import os
+import random
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from conftest import GOLDEN
+from oracle import (bypass_to_standard_ep, capacity_from_alpha, expert_loads,
+                    least_loaded_assignment, min_max_load_exhaustive, pair_ranks,
+                    permute, plan, standard_ep_assignment)
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# --------------------------------------------------------------------------
+# worked example of Sec. 2.1
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("P,mode", [(1, "llep"), (2, "ep"), (4, "ep"), (8, "ep")])
+def test_reindex_worked_example(P, mode):
+    g = _load("reindex_example.json")
+    ids = g["ids"]
+    E = 8
+    pl = plan(ids, E, P, cap=len(ids), m=1, mode=mode)
+    pair_row, row_pair = permute(ids, pl, E)
+    names = g["tokens"]
+    assert [names[p] for p in row_pair] == g["reindexed"]
+    for e, members in g["groups"].items():
+        rows = [r for r in range(len(row_pair)) if ids[row_pair[r]] == int(e)]
+        assert [names[row_pair[r]] for r in rows] == members
+        assert rows == list(range(rows[0], rows[0] + len(rows)))  # contiguous
+
+
+# --------------------------------------------------------------------------
+# hand traces of Alg. 2 / Alg. 3
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("trace", _load("lla_hand_traces.json")["traces"],
+                         ids=lambda t: t["name"].split()[0])
+def test_lla_hand_trace(trace):
+    loads, P = trace["loads"], trace["P"]
+    M = len(loads) // P
+    A, W, forced = least_loaded_assignment(loads, M, trace["cap"], trace["m"])
+    got = {str(e): [list(c) for c in A.get(e, [])] for e in range(len(loads))}
+    assert got == trace["assignments"]
+    assert [list(w) for w in W] == trace["transfers"]
+    assert forced == trace["forced"]
+    ids = [e for e, l in enumerate(loads) for _ in range(l)]
+    pl = plan(ids, len(loads), P, trace["cap"], trace["m"])
+    assert pl.device_rows == trace["device_rows"]
+    assert [list(t) for t in pl.transfers] == trace["transfers"]
+    if "groups" in trace:
+        assert [list(g) for g in pl.groups] == trace["groups"]
+
+
+# --------------------------------------------------------------------------
+# capacity (Alg. 2, m_alpha) on the five layer shapes
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("R,alpha,P,cap", [
+    (256 * 2, Fraction(5, 4), 4, 160),
+    (16384 * 4, Fraction(11, 10), 8, 9012),
+    (32768 * 4, Fraction(11, 10), 8, 18023),
+    (65536 * 8, Fraction(11, 10), 8, 72090),
+    (8192 * 8, Fraction(1), 8, 8192),
+])
+def test_capacity_values(R, alpha, P, cap):
+    assert capacity_from_alpha(R, alpha, P) == cap
+
+
+# --------------------------------------------------------------------------
+# lambda bypass (Alg. 4)
+# --------------------------------------------------------------------------
+
+def test_bypass_rule():
+    assert bypass_to_standard_ep([3, 3, 3, 3], 1.3)          # max/mean = 1
+    assert not bypass_to_standard_ep([6, 2, 2, 2], 1.3)      # max/mean = 2
+    assert not bypass_to_standard_ep([4, 0, 2, 2], 2.0)      # equal: strict <
+    assert bypass_to_standard_ep([4, 0, 2, 2], 2.0000001)
+    assert not bypass_to_standard_ep([3, 3, 3, 3], 0.0)      # disabled
+    assert not bypass_to_standard_ep([0, 0, 0, 0], 1.3)      # no pairs
+
+
+def test_plan_bypass_gives_ep_plan():
+    ids = [0, 1, 2, 3, 0, 1, 2, 3, 0, 0]
+    pl = plan(ids, 4, 2, cap=5, m=1, mode="llep", lam=10.0)
+    ep = plan(ids, 4, 2, cap=5, m=1, mode="ep")
+    assert pl.bypassed and pl.chunks == ep.chunks and pl.groups == ep.groups
+
+
+# --------------------------------------------------------------------------
+# invariants over random loads (hypothesis)
+# --------------------------------------------------------------------------
+
+@st.composite
+def _plan_case(draw):
+    P = draw(st.integers(1, 6))
+    M = draw(st.integers(1, 5))
+    E = P * M
+    loads = draw(st.lists(st.integers(0, 40), min_size=E, max_size=E))
+    R = sum(loads)
+    base = math.ceil(R / P)
+    cap = base + draw(st.integers(0, 10))
+    return loads, P, M, cap
+
+
+def _check_tiles(A, loads):
+    """Every expert's chunks tile [0, l_e) exactly once, in start order."""
+    for e, l in enumerate(loads):
+        chunks = sorted(A.get(e, []), key=lambda c: c[1])
+        pos = 0
+        for (d, s, t) in chunks:
+            assert s == pos and t > s
+            pos = t
+        assert pos == l
+
+
+@settings(max_examples=400, deadline=None)
+@given(_plan_case())
+def test_lla_invariants_m1(case):
+    loads, P, M, cap = case
+    E = P * M
+    A, W, forced = least_loaded_assignment(loads, M, cap, 1)
+    _check_tiles(A, loads)
+    rows = [0] * P
+    nchunks = 0
+    for e, chunks in A.items():
+        for (d, s, t) in chunks:
+            rows[d] += t - s
+            nchunks += 1
+    # conservation
+    assert sum(rows) == sum(loads)
+    # capacity: with m = 1 and P * cap >= R no device exceeds cap, no force
+    assert max(rows) <= cap and forced == 0
+    # chunk bound: <= 1 native + 1 final spill per expert, <= P filling spills
+    assert nchunks <= 2 * E + P
+    # transfers are exactly the foreign (expert, device) pairs
+    foreign = {(e, e // M, d) for e, cs in A.items() for (d, s, t) in cs
+               if d != e // M}
+    assert set(W) == foreign and W == sorted(W)
+    # native first: a device whose native load fits keeps its experts whole
+    g_n = [sum(loads[d * M:(d + 1) * M]) for d in range(P)]
+    for e in range(E):
+        if g_n[e // M] <= cap and loads[e] > 0:
+            assert A[e] == [(e // M, 0, loads[e])]
+    # EP degeneracy: plan == standard EP iff every native load fits
+    ep = standard_ep_assignment(loads, M)
+    same = all(A.get(e, []) == ep[e] for e in range(E))
+    assert same == (max(g_n) <= cap)
+
+
+@settings(max_examples=300, deadline=None)
+@given(_plan_case(), st.integers(1, 12))
+def test_lla_invariants_any_m(case, m):
+    loads, P, M, cap = case
+    E = P * M
+    A, W, forced = least_loaded_assignment(loads, M, cap, m)
+    _check_tiles(A, loads)
+    nchunks = sum(len(c) for c in A.values())
+    assert nchunks <= 2 * E + P
+    # every spilled (non-native) chunk smaller than m is the expert's last one
+    for e, cs in A.items():
+        cs = sorted(cs, key=lambda c: c[1])
+        for i, (d, s, t) in enumerate(cs):
+            if d != e // M and t - s < m:
+                assert i == len(cs) - 1
+
+
+# --------------------------------------------------------------------------
+# exhaustive optimum on tiny inputs
+# --------------------------------------------------------------------------
+
+def test_exhaustive_optimum():
+    rng = random.Random(0)
+    cases = 0
+    while cases < 60:
+        P = rng.choice([2, 3])
+        M = rng.choice([1, 2]) if P == 2 else 1
+        E = P * M
+        loads = [rng.randint(0, 6) for _ in range(E)]
+        R = sum(loads)
+        if R == 0:
+            continue
+        cases += 1
+        opt, _ = min_max_load_exhaustive(loads, P, M)
+        assert opt == math.ceil(R / P)  # closed form of the integer optimum
+        A, _, _ = least_loaded_assignment(loads, M, math.ceil(R / P), 1)
+        rows = [0] * P
+        for cs in A.values():
+            for (d, s, t) in cs:
+                rows[d] += t - s
+        assert max(rows) == opt
+        # with a looser cap LLA stays between the optimum and the cap
+        cap = math.ceil(R / P) + rng.randint(0, 3)
+        A, _, _ = least_loaded_assignment(loads, M, cap, 1)
+        rows = [0] * P
+        for cs in A.values():
+            for (d, s, t) in cs:
+                rows[d] += t - s
+        assert opt <= max(rows) <= cap
+
+
+# --------------------------------------------------------------------------
+# loads, ranks and the permutation
+# --------------------------------------------------------------------------
+
+def test_loads_match_bincount_and_flag_bad_ids():
+    rng = np.random.default_rng(1)
+    ids = rng.integers(0, 12, size=500)
+    loads, status = expert_loads(ids, 12)
+    assert loads == np.bincount(ids, minlength=12).tolist() and status == 0
+    loads, status = expert_loads([0, 5, -1, 12, 3], 12)
+    assert status == 1 and sum(loads) == 3
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_ep_permutation_is_stable_sort(seed):
+    rng = np.random.default_rng(seed)
+    E, P = 16, 4
+    ids = rng.integers(0, E, size=300)
+    pl = plan(ids, E, P, cap=10**6, mode="ep")
+    pair_row, row_pair = permute(ids, pl, E)
+    assert np.array_equal(row_pair, np.argsort(ids, kind="stable"))
+    assert np.array_equal(pair_row[row_pair], np.arange(300))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_llep_permutation_structure(seed):
+    rng = np.random.default_rng(seed)
+    E, P = 12, 3
+    R = 400
+    ids = np.where(rng.random(R) < 0.7, 0, rng.integers(0, E, size=R))
+    cap = math.ceil(R / P)
+    pl = plan(ids, E, P, cap=cap, m=1)
+    pair_row, row_pair = permute(ids, pl, E)
+    # a bijection between pairs and rows
+    assert sorted(pair_row.tolist()) == list(range(R))
+    assert np.array_equal(row_pair[pair_row], np.arange(R))
+    ranks = pair_ranks(ids, E)
+    for (d, e, row0, n) in pl.groups:
+        ps = row_pair[row0:row0 + n]
+        assert all(ids[p] == e for p in ps)
+        assert list(ps) == sorted(ps)  # pair order kept inside a group
+    # rows of device d are [sum(rows before d), + device_rows[d])
+    start = 0
+    for d in range(P):
+        for g in pl.groups[pl.group_begin[d]:pl.group_begin[d + 1]]:
+            assert g[0] == d and start <= g[2] < start + pl.device_rows[d]
+        start += pl.device_rows[d]
+    # a chunk holds the expert's pairs with rank in [start, end)
+    for c, (d, e, s, t) in enumerate(pl.chunks):
+        ps = row_pair[pl.chunk_row[c]:pl.chunk_row[c] + (t - s)]
+        assert [ranks[p] for p in ps] == list(range(s, t))
+
+
+def test_invalid_ids_get_no_row():
+    ids = [0, 1, 7, 1, -3, 0]
+    pl = plan(ids, 4, 2, cap=3)
+    pair_row, row_pair = permute(ids, pl, 4)
+    assert pl.status == 1
+    assert pair_row[2] == -1 and pair_row[4] == -1
+    assert sum(pl.device_rows) == 4
