@@ -1,0 +1,234 @@
+// C ABI of the LLEP hot path: argument checks on the host, then launches.
+// No entry point allocates, synchronizes or keeps state between calls
+// (apart from the calling thread's last error text).
+#include <stdint.h>
+#include <string.h>
+
+#include <string>
+
+#include "kernels.h"
+#include "llep.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string &msg) {
+  g_last_error = msg;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return LLEP_OK;
+}
+
+int hip_result(hipError_t err, const char *where) {
+  if (err == hipSuccess) return ok();
+  return fail(LLEP_E_HIP, std::string(where) + ": " + hipGetErrorString(err));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_params(const llep_plan_params *p) {
+  if (!p) return fail(LLEP_E_ARG, "params is null");
+  if (p->T < 0) return fail(LLEP_E_ARG, "T < 0");
+  if (p->K < 1) return fail(LLEP_E_ARG, "K < 1");
+  if (p->E < 1 || p->E > LLEP_MAX_EXPERTS) return fail(LLEP_E_ARG, "E outside [1, LLEP_MAX_EXPERTS]");
+  if (p->P < 1 || p->P > LLEP_MAX_DEVICES) return fail(LLEP_E_ARG, "P outside [1, LLEP_MAX_DEVICES]");
+  if (p->E % p->P != 0) return fail(LLEP_E_ARG, "E % P != 0");
+  if (p->T > int64_t(INT32_MAX) / p->K) return fail(LLEP_E_ARG, "T * K >= 2^31");
+  if (p->capacity < 1) return fail(LLEP_E_ARG, "capacity < 1");
+  if (p->mode != LLEP_MODE_LLEP && p->mode != LLEP_MODE_EP) return fail(LLEP_E_ARG, "unknown mode");
+  if (p->reserved != 0) return fail(LLEP_E_ARG, "reserved field is not 0");
+  return LLEP_OK;
+}
+
+int check_plan_buffers(const llep_plan_buffers *b) {
+  if (!b) return fail(LLEP_E_ARG, "plan buffers are null");
+  if (!b->loads || !b->chunks || !b->chunk_row || !b->expert_chunk_begin || !b->groups ||
+      !b->group_begin || !b->device_rows || !b->xfers || !b->rank_base || !b->info)
+    return fail(LLEP_E_ARG, "a plan buffer pointer is null");
+  return LLEP_OK;
+}
+
+int elem_bytes(llep_dtype d) { return d == LLEP_BF16 ? 2 : (d == LLEP_F32 ? 4 : 0); }
+
+int check_rows(int32_t D, llep_dtype dtype) {
+  const int eb = elem_bytes(dtype);
+  if (eb == 0) return fail(LLEP_E_DTYPE, "unknown dtype");
+  if (D < 1) return fail(LLEP_E_ARG, "D < 1");
+  if (D % 8 != 0) return fail(LLEP_E_ARG, "D % 8 != 0 (rows must be whole 16-byte vectors)");
+  return LLEP_OK;
+}
+
+int check_ffn_dims(int32_t D, int32_t F, llep_dtype dtype) {
+  if (elem_bytes(dtype) == 0) return fail(LLEP_E_DTYPE, "unknown dtype");
+  if (D < 64 || D % 64 != 0) return fail(LLEP_E_ARG, "D must be a positive multiple of 64");
+  if (F < 64 || F % 64 != 0) return fail(LLEP_E_ARG, "F must be a positive multiple of 64");
+  return LLEP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *llep_last_error(void) { return g_last_error.c_str(); }
+
+int32_t llep_plan_max_chunks(const llep_plan_params *params) {
+  if (check_params(params) != LLEP_OK) return -1;
+  return 2 * params->E + params->P;
+}
+
+int64_t llep_plan_rank_base_elems(const llep_plan_params *params) {
+  if (check_params(params) != LLEP_OK) return -1;
+  const int64_t tiles = llep::rank_tiles(params->T * params->K);
+  return tiles * params->E + tiles;
+}
+
+int llep_plan(const llep_plan_params *params, const int32_t *topk_ids,
+              const llep_plan_buffers *out, hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if ((rc = check_plan_buffers(out)) != LLEP_OK) return rc;
+  const int64_t R = params->T * params->K;
+  if (R > 0 && !topk_ids) return fail(LLEP_E_ARG, "topk_ids is null");
+  llep::PlanArgs a;
+  a.R = R;
+  a.E = params->E;
+  a.P = params->P;
+  a.M = params->E / params->P;
+  a.min_chunk = params->min_chunk < 1 ? 1 : params->min_chunk;
+  a.mode = params->mode;
+  a.cap = params->capacity;
+  a.lambda = params->lambda;
+  a.n_tiles = int32_t(llep::rank_tiles(R));
+  a.ids = topk_ids;
+  a.buf = *out;
+  return hip_result(llep::launch_plan(a, stream), "llep_plan");
+}
+
+int llep_permute(const llep_plan_params *params, const llep_plan_buffers *plan,
+                 const int32_t *topk_ids, const float *topk_gates, const void *x, int32_t D,
+                 llep_dtype dtype, void *x_perm, float *gate_perm, int32_t *row_pair,
+                 int32_t *pair_row, hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if ((rc = check_plan_buffers(plan)) != LLEP_OK) return rc;
+  if ((rc = check_rows(D, dtype)) != LLEP_OK) return rc;
+  if (params->T > 0 &&
+      (!topk_ids || !topk_gates || !x || !x_perm || !gate_perm || !row_pair || !pair_row))
+    return fail(LLEP_E_ARG, "a data pointer is null");
+  if (!aligned16(x) || !aligned16(x_perm)) return fail(LLEP_E_ARG, "x / x_perm not 16-byte aligned");
+  llep::PermuteArgs a;
+  a.T = params->T;
+  a.R = params->T * params->K;
+  a.K = params->K;
+  a.E = params->E;
+  a.D = D;
+  a.n_tiles = int32_t(llep::rank_tiles(a.R));
+  a.elem_bytes = elem_bytes(dtype);
+  a.ids = topk_ids;
+  a.gates = topk_gates;
+  a.x = x;
+  a.x_perm = x_perm;
+  a.gate_perm = gate_perm;
+  a.row_pair = row_pair;
+  a.pair_row = pair_row;
+  a.plan = *plan;
+  return hip_result(llep::launch_permute(a, stream), "llep_permute");
+}
+
+size_t llep_packed_gate_up_bytes(int32_t E, int32_t D, int32_t F, llep_dtype dtype) {
+  if (E < 1 || D < 1 || F < 1 || elem_bytes(dtype) == 0) return 0;
+  return size_t(E) * 2 * size_t(F) * size_t(D) * elem_bytes(dtype);
+}
+
+size_t llep_packed_down_bytes(int32_t E, int32_t D, int32_t F, llep_dtype dtype) {
+  if (E < 1 || D < 1 || F < 1 || elem_bytes(dtype) == 0) return 0;
+  return size_t(E) * size_t(D) * size_t(F) * elem_bytes(dtype);
+}
+
+int llep_pack_weights(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const void *w_gate,
+                      const void *w_up, const void *w_down, void *w_gate_up_packed,
+                      void *w_down_packed, hipStream_t stream) {
+  if (E < 1 || E > LLEP_MAX_EXPERTS) return fail(LLEP_E_ARG, "E outside [1, LLEP_MAX_EXPERTS]");
+  int rc = check_ffn_dims(D, F, dtype);
+  if (rc != LLEP_OK) return rc;
+  if (!w_gate || !w_up || !w_down || !w_gate_up_packed || !w_down_packed)
+    return fail(LLEP_E_ARG, "a weight pointer is null");
+  if (!aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) ||
+      !aligned16(w_gate_up_packed) || !aligned16(w_down_packed))
+    return fail(LLEP_E_ARG, "weights not 16-byte aligned");
+  return hip_result(llep::launch_pack(E, D, F, dtype, w_gate, w_up, w_down, w_gate_up_packed,
+                                      w_down_packed, stream),
+                    "llep_pack_weights");
+}
+
+size_t llep_grouped_ffn_workspace_bytes(const llep_plan_params *params, int32_t F,
+                                        llep_dtype dtype) {
+  if (check_params(params) != LLEP_OK || F < 1 || elem_bytes(dtype) == 0) return 0;
+  return llep::ffn_workspace_bytes(params->T * params->K, params->E, params->P, F, dtype);
+}
+
+int llep_grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *plan,
+                     int32_t device, const void *x_perm, const void *w_gate_up_packed,
+                     const void *w_down_packed, int32_t D, int32_t F, llep_dtype dtype,
+                     void *out_perm, void *workspace, size_t workspace_bytes,
+                     hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if ((rc = check_plan_buffers(plan)) != LLEP_OK) return rc;
+  if ((rc = check_ffn_dims(D, F, dtype)) != LLEP_OK) return rc;
+  if (device < -1 || device >= params->P) return fail(LLEP_E_ARG, "device outside [-1, P)");
+  if (!x_perm || !w_gate_up_packed || !w_down_packed || !out_perm)
+    return fail(LLEP_E_ARG, "a data pointer is null");
+  if (!aligned16(x_perm) || !aligned16(w_gate_up_packed) || !aligned16(w_down_packed) ||
+      !aligned16(out_perm))
+    return fail(LLEP_E_ARG, "data not 16-byte aligned");
+  const size_t need = llep::ffn_workspace_bytes(params->T * params->K, params->E, params->P, F, dtype);
+  if (!workspace || workspace_bytes < need)
+    return fail(LLEP_E_WORKSPACE, "workspace missing or smaller than llep_grouped_ffn_workspace_bytes");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(LLEP_E_WORKSPACE, "workspace not 256-byte aligned");
+  llep::FfnArgs a;
+  a.R = params->T * params->K;
+  a.P = params->P;
+  a.E = params->E;
+  a.D = D;
+  a.F = F;
+  a.device = device;
+  a.dtype = dtype;
+  a.groups = plan->groups;
+  a.group_begin = plan->group_begin;
+  a.x_perm = x_perm;
+  a.w_gate_up = w_gate_up_packed;
+  a.w_down = w_down_packed;
+  a.out_perm = out_perm;
+  a.ws = workspace;
+  a.ws_bytes = workspace_bytes;
+  return hip_result(llep::launch_grouped_ffn(a, stream), "llep_grouped_ffn");
+}
+
+int llep_combine(const llep_plan_params *params, const void *out_perm, const int32_t *pair_row,
+                 const float *topk_gates, int32_t D, llep_dtype dtype, void *y,
+                 hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if ((rc = check_rows(D, dtype)) != LLEP_OK) return rc;
+  if (params->T > 0 && (!out_perm || !pair_row || !topk_gates || !y))
+    return fail(LLEP_E_ARG, "a data pointer is null");
+  if (!aligned16(out_perm) || !aligned16(y)) return fail(LLEP_E_ARG, "out_perm / y not 16-byte aligned");
+  llep::CombineArgs a;
+  a.T = params->T;
+  a.K = params->K;
+  a.D = D;
+  a.dtype = dtype;
+  a.out_perm = out_perm;
+  a.pair_row = pair_row;
+  a.gates = topk_gates;
+  a.y = y;
+  return hip_result(llep::launch_combine(a, stream), "llep_combine");
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Internal launch interface between the C ABI (abi.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "llep.h"
+
+namespace llep {
+
+constexpr int kMaxChunks = 2 * LLEP_MAX_EXPERTS + LLEP_MAX_DEVICES;
+
+// Internal status bit: the plan tables overflowed (never expected; the chunk
+// count is bounded by 2E + P).
+constexpr int32_t kStatusPlanOverflow = 1 << 30;
+
+int64_t rank_tiles(int64_t R);
+
+struct PlanArgs {
+  int64_t R;
+  int32_t E, P, M, min_chunk, mode;
+  int64_t cap;
+  double lambda;
+  int32_t n_tiles;
+  const int32_t *ids;
+  llep_plan_buffers buf;
+};
+hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
+
+struct PermuteArgs {
+  int64_t T, R;
+  int32_t K, E, D;
+  int32_t n_tiles;
+  int32_t elem_bytes;
+  const int32_t *ids;
+  const float *gates;
+  const void *x;
+  void *x_perm;
+  float *gate_perm;
+  int32_t *row_pair, *pair_row;
+  llep_plan_buffers plan;
+};
+hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream);
+
+struct CombineArgs {
+  int64_t T;
+  int32_t K, D;
+  llep_dtype dtype;
+  const void *out_perm;
+  const int32_t *pair_row;
+  const float *gates;
+  void *y;
+};
+hipError_t launch_combine(const CombineArgs &a, hipStream_t stream);
+
+struct FfnArgs {
+  int64_t R;
+  int32_t P, E, D, F, device;
+  llep_dtype dtype;
+  const int32_t *groups, *group_begin;
+  const void *x_perm, *w_gate_up, *w_down;
+  void *out_perm;
+  void *ws;
+  size_t ws_bytes;
+};
+size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t F,
+                           llep_dtype dtype);
+hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream);
+
+hipError_t launch_pack(int32_t E, int32_t D, int32_t F, llep_dtype dtype,
+                       const void *w_gate, const void *w_up,
+                       const void *w_down, void *gu, void *dn,
+                       hipStream_t stream);
+
+}  // namespace llep

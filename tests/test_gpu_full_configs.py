@@ -1,0 +1,154 @@
+"""GPU parity at the full sizes of the five layer shapes (and the gpt-oss-120b
+hot-set sweep): plan and permutation bit-exact against the oracle; expert
+outputs on sampled rows and tokens the oracle computes one by one; the
+single-device launch the benchmark times."""
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import LayerRun, assert_plan_equal, device, rel_err
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+TOL_BF16 = 2e-2
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+def _cfg(name):
+    from paper_2601_17111_amd.synth import CONFIGS, gpt_oss_120b
+    if name.startswith("gpt-oss-120b-hot"):
+        return gpt_oss_120b(int(name[len("gpt-oss-120b-hot"):]))
+    return CONFIGS[name]
+
+
+PLAN_CASES = ([("gpt-oss-20b", 0), ("qwen3-30b-a3b", 0), ("deepseek-v3", 0)] +
+              [(f"gpt-oss-120b-hot{k}", s) for k in (16, 4, 1) for s in (0, 1, 2)])
+
+
+@pytest.mark.parametrize("name,seed", PLAN_CASES, ids=lambda v: str(v))
+def test_full_plan_and_permutation(dev, name, seed):
+    import torch
+    cfg = _cfg(name)
+    run = LayerRun(cfg, seed, dev, weights=False)
+    L = run.layer
+    flat = run.inp.ids.reshape(-1).tolist()
+    for mode in ("llep", "ep"):
+        L.set_mode(mode)
+        L.plan(run.ids)
+        L.permute(run.ids, run.gates, run.x)
+        torch.cuda.synchronize()
+        ref = oracle.plan(flat, cfg.E, cfg.P, cfg.capacity, cfg.min_chunk, mode=mode)
+        info = L.bufs.info_dict()
+        nc, ng, nx = info["n_chunks"], info["n_groups"], info["n_xfers"]
+        got = dict(
+            loads=L.bufs.loads.cpu().tolist(),
+            chunks=[tuple(c) for c in L.bufs.chunks[:nc].cpu().tolist()],
+            chunk_row=L.bufs.chunk_row[:nc].cpu().tolist(),
+            expert_chunk_begin=L.bufs.expert_chunk_begin.cpu().tolist(),
+            groups=[tuple(g) for g in L.bufs.groups[:ng].cpu().tolist()],
+            group_begin=L.bufs.group_begin.cpu().tolist(),
+            device_rows=L.bufs.device_rows.cpu().tolist(),
+            transfers=[tuple(x) for x in L.bufs.xfers[:nx].cpu().tolist()])
+        assert_plan_equal(got, info, ref)
+        if mode == "llep":
+            # capacity holds (m = 1, P * cap >= R)
+            assert max(ref.device_rows) <= cfg.capacity
+        pr_ref, rp_ref = oracle.permute(flat, ref, cfg.E)
+        assert np.array_equal(L.pair_row.cpu().numpy(), pr_ref)
+        n = info["total_rows"]
+        assert np.array_equal(L.row_pair[:n].cpu().numpy(), rp_ref)
+        rp = torch.from_numpy(rp_ref.astype(np.int64))
+        assert torch.equal(L.gate_perm[:n].cpu(), run.gates.reshape(-1).cpu()[rp])
+        # x_perm rows: bit copies of their token rows (sampled)
+        rng = np.random.default_rng(seed)
+        rows = np.unique(np.concatenate([rng.integers(0, n, 2048), [0, n - 1]]))
+        rows_t = torch.from_numpy(rows).to(dev)
+        src = torch.from_numpy(rp_ref[rows] // cfg.K).to(dev)
+        assert torch.equal(L.x_perm[rows_t], run.x[src])
+
+
+def _expert_subset(cfg, ids, n_extra, rng):
+    loads = np.bincount(ids.reshape(-1), minlength=cfg.E)
+    order = np.argsort(-loads, kind="stable")
+    hot = [int(e) for e in order[:max(1, n_extra // 2)]]
+    rest = [int(e) for e in rng.permutation(order[len(hot):])[:n_extra - len(hot)]]
+    return sorted(set(hot + rest))
+
+
+FFN_CASES = ["gpt-oss-20b", "gpt-oss-120b-hot16", "gpt-oss-120b-hot4", "gpt-oss-120b-hot1",
+             "qwen3-30b-a3b", "deepseek-v3"]
+
+
+@pytest.mark.parametrize("name", FFN_CASES)
+def test_full_layer_outputs(dev, name):
+    import torch
+    cfg = _cfg(name)
+    run = LayerRun(cfg, 0, dev)
+    rng = np.random.default_rng(7)
+    y = run.forward(-1).float().cpu().numpy()
+    L = run.layer
+    ids = run.inp.ids
+    flat = ids.reshape(-1)
+    S = _expert_subset(cfg, ids, 24 if cfg.E > 32 else cfg.E, rng)
+    W = run.host_weights(S)
+    info = L.bufs.info_dict()
+    groups = L.bufs.groups[:info["n_groups"]].cpu().numpy()
+    row_pair = L.row_pair[:info["total_rows"]].cpu().numpy()
+    out = L.out_perm
+    # rows of every group of a sampled expert: first, last and one inside
+    checked = 0
+    for (d, e, r0, n) in groups:
+        if int(e) not in W:
+            continue
+        rows = sorted({int(r0), int(r0 + n - 1), int(r0 + rng.integers(0, n))})
+        o = out[torch.tensor(rows, device=dev)].float().cpu().numpy()
+        xs = run.inp.x[row_pair[rows] // cfg.K]
+        want = oracle.swiglu_ffn(xs, *W[int(e)])
+        err = rel_err(o, want)
+        assert err <= TOL_BF16, f"group ({d},{e}) rows {rows}: {err:.3e}"
+        checked += 1
+    assert checked > 0
+    # tokens whose experts are all sampled: boundary tokens first, then random
+    ok_tok = np.all(np.isin(ids, S), axis=1)
+    cand = np.nonzero(ok_tok)[0]
+    assert len(cand) > 0
+    chunks = L.bufs.chunks[:info["n_chunks"]].cpu().numpy()
+    chunk_row = L.bufs.chunk_row[:info["n_chunks"]].cpu().numpy()
+    boundary = set()
+    for (d, e, s, t), r in zip(chunks, chunk_row):
+        for rr in (int(r), int(r + t - s - 1)):
+            tok = int(row_pair[rr]) // cfg.K
+            if ok_tok[tok]:
+                boundary.add(tok)
+    sample = sorted(boundary)[:96]
+    sample += [int(t) for t in rng.choice(cand, size=min(64, len(cand)), replace=False)]
+    sample = sorted(set(sample))
+    want = oracle.moe_output(run.inp.x, ids, run.inp.gates, lambda e: W.get(e), sample)
+    err = rel_err(y[sample], want)
+    assert err <= TOL_BF16, f"y relative error {err:.3e}"
+    # the benchmark's launch: only the most loaded device's groups
+    dstar = info["max_device"]
+    starts = np.concatenate([[0], np.cumsum(L.bufs.device_rows.cpu().numpy())])
+    a, b = int(starts[dstar]), int(starts[dstar + 1])
+    ref_rows = out[a:b].clone()
+    out[a:b].zero_()
+    L.ffn(run.gu, run.dn, dstar)
+    torch.cuda.synchronize()
+    assert torch.equal(out[a:b], ref_rows)
+    del flat
+
+
+def test_full_ep_equals_llep_bitwise(dev):
+    cfg = _cfg("gpt-oss-120b-hot1")
+    run = LayerRun(cfg, 0, dev)
+    y_llep = run.forward(-1).clone()
+    assert run.layer.bufs.info_dict()["n_xfers"] > 0
+    run.layer.set_mode("ep")
+    y_ep = run.forward(-1)
+    import torch
+    assert torch.equal(y_llep, y_ep)
