@@ -1,0 +1,278 @@
+"""Benchmark of the LLEP expert-layer hot path on one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic input, all
+on one stream: plan (histogram + least-loaded assignment) -> permute ->
+grouped SwiGLU FFN of the most-loaded virtual device's groups -> combine.
+Inputs are resident in HBM before timing starts; the most-loaded device d* is
+read from the plan once, before timing (the batch does not change).
+
+Prints one JSON line. `value` is tokens per second of the measured step
+(T / time per step). The `roofline` object is for the grouped FFN (two MFMA
+GEMM kernels plus a tiny tile-list kernel): algorithmic flops 6*D*F per row of
+d*, over the average duration of that call measured with HIP events on its
+stream. `cpu_baseline` times the CPU oracle on a bounded sample of the same
+workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s + grouped-GEMM % bf16 MFMA peak, max-loaded share, 1 GPU"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (vendor figure)
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E (vendor figure)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "grouped_ffn_traffic.json")
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gpt-oss-120b-hot1")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-sample-rows", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ep", action="store_true", help="skip the standard-EP comparison")
+    return ap.parse_args()
+
+
+def _config(name):
+    from paper_2601_17111_amd.synth import CONFIGS, gpt_oss_120b
+    if name.startswith("gpt-oss-120b-hot"):
+        return gpt_oss_120b(int(name[len("gpt-oss-120b-hot"):]))
+    return CONFIGS[name]
+
+
+def _kernel_hash():
+    h = hashlib.sha256()
+    for f in ("grouped_ffn.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2601_17111_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic(workload):
+    """Measured HBM bytes per grouped-FFN call from the committed counter
+    summary, if it was taken on this workload with the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_hash") != _kernel_hash() or t.get("workload") != workload:
+        return None
+    return t.get("bytes_per_call")
+
+
+def _time_steps(layer, run, steps, dstar):
+    """Run `steps` steps; per-segment HIP event times (ms) on the stream."""
+    import torch
+    seg = {"plan": 0.0, "permute": 0.0, "grouped_ffn": 0.0, "combine": 0.0}
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        e = ev[i]
+        e[0].record()
+        layer.plan(run["ids"])
+        e[1].record()
+        layer.permute(run["ids"], run["gates"], run["x"])
+        e[2].record()
+        layer.ffn(run["gu"], run["dn"], dstar)
+        e[3].record()
+        layer.combine(run["gates"])
+        e[4].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for e in ev:
+        for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
+            seg[k] += a.elapsed_time(b) / steps
+    return wall * 1e3 / steps, seg
+
+
+def _cpu_baseline(cfg, inp, expert_weights, args):
+    """The oracle on the host: plan and permutation over all pairs (pure
+    Python, one core), the SwiGLU expert function (float64 numpy BLAS) over a
+    sample of the most-loaded device's rows scaled to all of them, and the
+    gate-weighted sum over a sample of tokens scaled to all tokens."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas = 1
+    flat = inp.ids.reshape(-1).tolist()
+    t0 = time.perf_counter()
+    pl = oracle.plan(flat, cfg.E, cfg.P, cfg.capacity, cfg.min_chunk, lam=cfg.lam)
+    t_plan = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    _, row_pair = oracle.permute(flat, pl, cfg.E)
+    t_perm = time.perf_counter() - t0
+    dstar = pl.max_device
+    groups = pl.groups[pl.group_begin[dstar]:pl.group_begin[dstar + 1]]
+    n_rows = pl.device_rows[dstar]
+    # sample rows of d*, spread over its groups in proportion to their size
+    rng = np.random.default_rng(0)
+    row0 = groups[0][2] if groups else 0
+    rows = row0 + np.sort(rng.choice(n_rows, size=min(args.cpu_sample_rows, n_rows), replace=False))
+    weights = {int(e): expert_weights(int(e)) for (_, e, _, _) in groups}
+    t0 = time.perf_counter()
+    for (d, e, r0, n) in groups:
+        sel = rows[(rows >= r0) & (rows < r0 + n)]
+        if len(sel) == 0:
+            continue
+        xs = inp.x[row_pair[sel] // cfg.K]
+        oracle.swiglu_ffn(xs, *weights[int(e)])
+    t_ffn = (time.perf_counter() - t0) * n_rows / max(1, len(rows))
+    ns = min(4096, cfg.T)
+    pair_out = rng.standard_normal((ns, cfg.K, cfg.D))
+    t0 = time.perf_counter()
+    oracle.combine(pair_out, inp.gates[:ns])
+    t_comb = (time.perf_counter() - t0) * cfg.T / ns
+    total = t_plan + t_perm + t_ffn + t_comb
+    return {
+        "value": cfg.T / total, "unit": "tokens/s", "cores": int(max(1, blas)),
+        "kind": "oracle",
+        "sample": (f"plan + permutation over all {cfg.R} pairs (pure Python, 1 core); "
+                   f"float64 SwiGLU over {len(rows)} of the {n_rows} rows of the most-loaded "
+                   f"device, scaled to all of them (numpy BLAS, {blas} threads); gate-weighted "
+                   f"sum over {ns} of {cfg.T} tokens, scaled"),
+        "seconds": {"plan": t_plan, "permute": t_perm, "ffn_scaled": t_ffn,
+                    "combine_scaled": t_comb},
+        "host_cores": len(os.sched_getaffinity(0)),
+    }
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the P devices of the "
+              f"plan are virtual devices on that GPU.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2601_17111_amd import binding as B
+    from paper_2601_17111_amd.layer import LLEPLayer
+    from paper_2601_17111_amd.synth import make_inputs, make_weights
+
+    B.lib()
+    dev = "cuda:0"
+    cfg = _config(args.workload)
+    inp = make_inputs(cfg, args.seed)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    run = dict(ids=torch.from_numpy(inp.ids).to(dev), gates=torch.from_numpy(inp.gates).to(dev),
+               x=torch.from_numpy(inp.x).to(dev).to(tdt))
+    wg, wu, wd = make_weights(cfg, args.seed, device=dev)
+    run["gu"], run["dn"] = B.llep_pack_weights(wg, wu, wd)
+    layer = LLEPLayer(cfg.T, cfg.K, cfg.E, cfg.P, cfg.D, cfg.F, cfg.capacity, tdt, dev,
+                      cfg.min_chunk, cfg.lam, "llep")
+
+    def plan_info():
+        layer.plan(run["ids"])
+        torch.cuda.synchronize()
+        info = layer.bufs.info_dict()
+        rows = layer.bufs.device_rows.cpu().tolist()
+        return info, rows
+
+    # untimed: the plan's most-loaded device and its groups
+    info, dev_rows = plan_info()
+    dstar = info["max_device"]
+    layer.permute(run["ids"], run["gates"], run["x"])
+    torch.cuda.synchronize()
+    n_rows = dev_rows[dstar]
+
+    for _ in range(args.warmup):
+        layer.plan(run["ids"])
+        layer.permute(run["ids"], run["gates"], run["x"])
+        layer.ffn(run["gu"], run["dn"], dstar)
+        layer.combine(run["gates"])
+    ms, seg = _time_steps(layer, run, args.steps, dstar)
+
+    D, F, T, K = cfg.D, cfg.F, cfg.T, cfg.K
+    eb = 2 if cfg.dtype == "bf16" else 4
+    flops = 6.0 * D * F * n_rows
+    tflops = flops / (seg["grouped_ffn"] * 1e-3) / 1e12
+    R = T * K
+    perm_bytes = T * D * eb + R * D * eb + 12 * R
+    comb_bytes = R * D * eb + T * D * eb + 8 * R
+    traffic = _traffic(args.workload)
+    out = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: MoE layer T={T} D={D} SwiGLU F={F} E={cfg.E} top-{K}, "
+                         f"P={cfg.P} virtual devices, capacity {cfg.capacity} "
+                         f"(alpha={cfg.alpha}), routing {cfg.routing}, seed {args.seed}; "
+                         f"step = plan + permute + grouped FFN of device {dstar} + combine"),
+            "global_batch": T, "parallelism": "1 GPU, P virtual devices",
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": tflops / PEAK_BF16_TFLOPS, "traffic": traffic,
+            "kernel": "llep_grouped_ffn on the most-loaded device (gemm_bf16_kernel x2 + tile list)",
+            "flops_per_launch": flops,
+        },
+        "segments_ms": seg,
+        "plan": {"max_device": dstar, "device_rows": dev_rows, "capacity": cfg.capacity,
+                 "n_chunks": info["n_chunks"], "n_groups": info["n_groups"],
+                 "n_xfers": info["n_xfers"]},
+        "permute_GBps": perm_bytes / (seg["permute"] * 1e-3) / 1e9,
+        "combine_GBps": comb_bytes / (seg["combine"] * 1e-3) / 1e9,
+    }
+    out["permute_hbm_frac"] = out["permute_GBps"] / PEAK_HBM_GBPS
+    out["combine_hbm_frac"] = out["combine_GBps"] / PEAK_HBM_GBPS
+    # P-device model of the layer: permute/combine are split evenly over the
+    # P source devices, the expert GEMMs wait for the most-loaded device
+    model_ms = seg["plan"] + (seg["permute"] + seg["combine"]) / cfg.P + seg["grouped_ffn"]
+    out["layer_tokens_per_s_p_device_model"] = T / (model_ms * 1e-3)
+
+    if not args.no_ep:
+        layer.set_mode("ep")
+        info_ep, rows_ep = plan_info()
+        d_ep = info_ep["max_device"]
+        layer.permute(run["ids"], run["gates"], run["x"])
+        for _ in range(2):
+            layer.ffn(run["gu"], run["dn"], d_ep)
+        ms_ep, seg_ep = _time_steps(layer, run, max(3, args.steps // 4), d_ep)
+        out["standard_ep"] = {
+            "max_device": d_ep, "max_device_rows": rows_ep[d_ep], "ms_per_step": ms_ep,
+            "segments_ms": seg_ep,
+            "grouped_ffn_TFLOPs": 6.0 * D * F * rows_ep[d_ep] / (seg_ep["grouped_ffn"] * 1e-3) / 1e12,
+        }
+        out["speedup_llep_vs_ep"] = {
+            "step": ms_ep / ms, "grouped_ffn": seg_ep["grouped_ffn"] / seg["grouped_ffn"]}
+        layer.set_mode("llep")
+
+    if not args.no_cpu_baseline:
+        def expert_weights(e):
+            return (wg[e].float().cpu().numpy(), wu[e].float().cpu().numpy(),
+                    wd[e].float().cpu().numpy())
+        out["cpu_baseline"] = _cpu_baseline(cfg, inp, expert_weights, args)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

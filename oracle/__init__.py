@@ -14,6 +14,7 @@ from .llep import (  # noqa: F401
     PlanResult,
     bypass_to_standard_ep,
     capacity_from_alpha,
+    combine,
     expert_loads,
     least_loaded_assignment,
     least_loaded_spill,

@@ -421,6 +421,13 @@ def moe_output(x: np.ndarray, ids: np.ndarray, gates: np.ndarray,
     return y
 
 
+def combine(pair_out: np.ndarray, gates: np.ndarray) -> np.ndarray:
+    """Eq. (1) given each pair's expert output: y[t] = sum_k gates[t, k] *
+    pair_out[t, k] (float64). pair_out: T x K x D; gates: T x K."""
+    return np.einsum("tk,tkd->td", np.asarray(gates, dtype=np.float64),
+                     np.asarray(pair_out, dtype=np.float64))
+
+
 # ---------------------------------------------------------------------------
 # Exhaustive optimum on tiny inputs (a pin for the plan's quality)
 # ---------------------------------------------------------------------------

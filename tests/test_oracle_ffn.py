@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 from conftest import GOLDEN
-from oracle import moe_output, silu, swiglu_ffn
+from oracle import combine, moe_output, silu, swiglu_ffn
 
 
 def test_silu_closed_forms():
@@ -101,3 +101,16 @@ def test_moe_output_token_subset_and_bad_ids():
     y2 = moe_output(x, ids2, gates, lambda e: W.get(e))
     want = np.float64(gates[0, 0]) * swiglu_ffn(x[:1], *W[ids[0, 0]])[0]
     assert np.allclose(y2[0], want, rtol=1e-14)
+
+
+def test_combine_matches_moe_output_and_closed_form():
+    bank, f0 = _expert_bank()
+    x = np.array([[1.0, 2.0], [1.0, 2.0]])
+    ids = np.array([[0, 2], [1, 0]])
+    gates = np.array([[0.5, 0.25], [1.0, 2.0]], dtype=np.float32)
+    pair_out = np.stack([np.stack([swiglu_ffn(x[t:t + 1], *bank[ids[t, k]])[0] for k in range(2)])
+                         for t in range(2)])
+    y = combine(pair_out, gates)
+    assert np.allclose(y[0], 0.5 * f0 + 0.25 * 2 * f0, rtol=1e-15)
+    assert np.allclose(y[1], 2.0 * f0, rtol=1e-15)
+    assert np.allclose(y, moe_output(x, ids, gates, lambda e: bank[e]), rtol=1e-14)
