@@ -6,13 +6,14 @@
 //   act = silu(X Wg_e) * (X Wu_e)      GEMM 1, SwiGLU fused in the epilogue
 //   out = act Wd_e                      GEMM 2
 //
-// bf16 path: persistent workgroups walk a tile list built on the device from
-// the group table (no host round trip). A tile never spans two groups. Tiles
-// are handed out so that the workgroups resident on one XCD (the hardware
-// deals workgroup ids round-robin over the 8 XCDs) work on neighbouring
-// tiles, which share operand panels in that XCD's L2. MFMA
-// v_mfma_f32_32x32x16_bf16 with fp32 accumulation; operand tiles are staged
-// in LDS (double-buffered, XOR-swizzled 16-byte chunks).
+// bf16 path: one persistent workgroup per CU walks a tile list built on the
+// device from the group table (no host round trip); a tile never spans two
+// groups. Tiles are handed out so that the workgroups resident on one XCD
+// (the hardware deals workgroup ids round-robin over the 8 XCDs) work on
+// neighbouring tiles, which share operand panels in that XCD's L2. Each tile
+// is 256 x BN, four waves of 128 x BN/2, v_mfma_f32_32x32x16_bf16 with fp32
+// accumulators in AGPRs; operands stream global -> LDS by DMA through a ring
+// of 32-deep k-slices, and MFMA fragments are double-buffered in registers.
 //
 // Packed weights (llep_pack_weights) keep the contraction dimension last, so
 // both GEMMs read 16-byte runs along K for A and B alike. In the gate/up
@@ -24,12 +25,11 @@
 
 namespace llep {
 
-constexpr int kBM = 128;
-constexpr int kBN = 128;
-constexpr int kBK = 64;
-constexpr int kWavesM = 2;
-constexpr int kWavesN = 2;
-constexpr int kGroupM = 8;  // m-tiles per super-row of the tile order
+constexpr int kTileM = 256;  // rows per GEMM tile (one m-tile never spans two groups)
+#ifndef LLEP_GROUP_M
+#define LLEP_GROUP_M 8
+#endif
+constexpr int kGroupM = LLEP_GROUP_M;  // m-tiles per super-row of the tile order
 
 struct WsLayout {
   size_t tiles_off, act_off, total;
@@ -38,7 +38,7 @@ struct WsLayout {
 
 static WsLayout ws_layout(int64_t R, int32_t E, int32_t P, int32_t F, llep_dtype dtype) {
   WsLayout L;
-  L.max_mtiles = R / kBM + (2 * int64_t(E) + P) + 1;
+  L.max_mtiles = R / kTileM + (2 * int64_t(E) + P) + 1;
   L.tiles_off = 256;
   const size_t tiles_bytes = (size_t(L.max_mtiles) * 8 + 255) / 256 * 256;
   L.act_off = L.tiles_off + tiles_bytes;
@@ -104,64 +104,196 @@ struct GemmArgs {
   int32_t N, Kdim;
 };
 
-__device__ __forceinline__ int lds_swz(int row, int kc) { return row * kBK + ((kc ^ (row & 7)) << 3); }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool kSwiglu>
-__global__ __launch_bounds__(64 * WAVES_M *WAVES_N) void gemm_bf16_kernel(GemmArgs g) {
-  constexpr int NT = 64 * WAVES_M * WAVES_N;
-  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+// ---------------------------------------------------------------------------
+// bf16 MFMA grouped GEMM, 256 x BN tiles, 4 waves of 128 x BN/2.
+//
+// Operand tiles move global -> LDS directly (global_load_lds_dwordx4: no VGPR
+// staging) in k-slices of 32, through a ring of 4 LDS stages with 3 slices
+// in flight, so each slice has three k-steps of MFMA work (~3000 cycles) to
+// arrive. Waits count outstanding DMA instructions (they complete in issue
+// order), one barrier per k-step.
+//
+// LDS stage layout: rows of 32 bf16 (64 B = 4 chunks of 16 B); chunk index
+// XORed with (row / 4) % 4. A ds_read_b128 serves 16 lanes per cycle from 64
+// four-byte banks; the fragment reads put 16 consecutive rows (4 rows per
+// 256-B bank line) in one group, and the XOR spreads them over all banks.
+// One DMA instruction fills 1 KB = 16 rows: lane l writes row l / 4, chunk
+// slot l % 4, so it loads logical chunk (l % 4) ^ ((l / 16) % 4).
+// ---------------------------------------------------------------------------
+
+typedef __attribute__((address_space(3))) void *lds_void_ptr;
+typedef __attribute__((address_space(1))) void *gbl_void_ptr;
+
+#ifndef LLEP_STAGES
+#define LLEP_STAGES 4
+#endif
+#ifndef LLEP_AHEAD
+#define LLEP_AHEAD 4
+#endif
+constexpr int kSK = 32;                // k-slice per LDS stage
+constexpr int kStages = LLEP_STAGES;   // LDS ring
+constexpr int kAhead = LLEP_AHEAD;     // slices requested ahead
+
+// The DMA is issued through asm so the compiler does not treat it as a
+// pending LDS write: it would otherwise wait for every DMA in flight before
+// each LDS read. The kernel orders DMA and reads itself (wait_cnt + barrier);
+// DMA completions are in issue order, so the compiler's own vmcnt waits for
+// other loads stay correct (they can only wait longer).
+__device__ __forceinline__ void dma16(const char *src, uint16_t *lds_block) {
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_ptr)(lds_block)));
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds), "v"(src)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited on)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// s_waitcnt vmcnt(VM) lgkmcnt(LGKM)
+template <int VM, int LGKM>
+__device__ __forceinline__ void wait_cnt() {
+  static_assert(VM >= 0 && VM < 64 && LGKM >= 0 && LGKM < 16, "waitcnt");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | 0x70 | (LGKM << 8));
+}
+
+__device__ __forceinline__ int lds_swz32(int row, int kc) {
+  return row * kSK + ((kc ^ ((row >> 2) & 3)) << 3);
+}
+
+struct TileCoord {
+  int e, row0, m0, rows_valid, n0, cols_valid;
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, int n_nt,
+                                            TileCoord &t) {
+  if (u >= n_mt * n_nt) return false;
+  const int sr = u / (kGroupM * n_nt);
+  const int rem = u - sr * (kGroupM * n_nt);
+  const int gm = min(kGroupM, n_mt - sr * kGroupM);
+  const int nt = rem / gm;
+  const int2 te = g.tiles[sr * kGroupM + rem % gm];
+  const int32_t *gr = g.groups + 4 * te.x;
+  t.e = gr[1];
+  t.row0 = gr[2];
+  t.m0 = te.y * BM;
+  t.rows_valid = min(BM, gr[3] - t.m0);
+  t.n0 = nt * BN;
+  t.cols_valid = min(BN, g.N - t.n0);
+  return true;
+}
+
+template <int BN, bool kSwiglu>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm256_kernel(GemmArgs g) {
+  constexpr int BM = 256;
+  constexpr int WM = 128, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int A_CH = BM * kBK / 8 / NT;  // 16-byte chunks per thread
-  constexpr int B_CH = BN * kBK / 8 / NT;
-  static_assert(A_CH * NT * 8 == BM * kBK && B_CH * NT * 8 == BN * kBK, "tile/thread mismatch");
+  constexpr int A_BLK = BM / 16 / 4;  // DMA instructions per wave per stage
+  constexpr int B_BLK = BN / 16 / 4;
+  constexpr int PER_STAGE = A_BLK + B_BLK;
+  static_assert((BN / 16) % 4 == 0, "BN");
+  static_assert(kAhead <= kStages && kAhead <= 4, "ring");
   static_assert(!kSwiglu || (WN % 64) == 0, "SwiGLU needs gate/up column pairs per wave");
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * kBK];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * kBK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sA[kStages][BM * kSK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB[kStages][BN * kSK];
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
   const int n_mt = *g.n_mtiles;
   const int n_nt = (g.N + BN - 1) / BN;
-  const int total = n_mt * n_nt;
   const int G = gridDim.x;  // a multiple of 8
   const int slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
-  const int nk = g.Kdim / kBK;
+  const int nk = g.Kdim / kSK;
+  const int kc_load = (lane & 3) ^ ((lane >> 4) & 3);
+  const int64_t lda_b = g.lda * 2, ldb_b = int64_t(g.Kdim) * 2;
+
+  TileCoord t;
+  if (!decode_tile<BM, BN>(g, slot, n_mt, n_nt, t)) return;
+  const char *Ab, *Bb;
+  int32_t a_off[A_BLK], b_off[B_BLK];
+  auto setup = [&](const TileCoord &c) {
+    Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
+    Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
+         int64_t(c.n0) * ldb_b;
+#pragma unroll
+    for (int j = 0; j < A_BLK; ++j) {
+      const int r = min((wave * A_BLK + j) * 16 + (lane >> 2), c.rows_valid - 1);
+      a_off[j] = int32_t(r * lda_b + kc_load * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < B_BLK; ++j) {
+      const int r = min((wave * B_BLK + j) * 16 + (lane >> 2), c.cols_valid - 1);
+      b_off[j] = int32_t(r * ldb_b + kc_load * 16);
+    }
+  };
+  auto issue = [&](int kt) {
+    const int st = kt % kStages;
+    const int kb = kt * kSK * 2;
+#pragma unroll
+    for (int j = 0; j < A_BLK; ++j) dma16(Ab + a_off[j] + kb, &sA[st][(wave * A_BLK + j) * 512]);
+#pragma unroll
+    for (int j = 0; j < B_BLK; ++j) dma16(Bb + b_off[j] + kb, &sB[st][(wave * B_BLK + j) * 512]);
+  };
+  auto prologue = [&]() {
+#pragma unroll
+    for (int k = 0; k < kAhead; ++k)
+      if (k < nk) issue(k);
+  };
+  setup(t);
+  prologue();
+
+  // MFMA operands of one 16-deep k-step: TM (A) and TN (B) 16-byte
+  // fragments per lane. Two sets alternate: the set for the next k-step is
+  // read from LDS while the current one feeds the MFMAs, so LDS latency hides
+  // behind 16 MFMAs.
+  static_assert(kSK == 32, "two k-steps per slice");
+  auto read_frags = [&](int kt, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
+    const uint16_t *a_s = sA[kt % kStages];
+    const uint16_t *b_s = sB[kt % kStages];
+    const int kc = ks * 2 + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      fa[i] = *reinterpret_cast<const bf16x8 *>(&a_s[lds_swz32(wm * WM + i * 32 + (lane & 31), kc)]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      fb[j] = *reinterpret_cast<const bf16x8 *>(&b_s[lds_swz32(wn * WN + j * 32 + (lane & 31), kc)]);
+  };
+  // Wait until slice kt is in LDS for every wave; slices requested after it
+  // may stay in flight. Each wave also finishes its own LDS reads first, so
+  // after the barrier the buffer of slice kt-1 (in registers everywhere) can
+  // be refilled.
+  auto wait_slice = [&](int kt) {
+    // requested so far: 0 .. kAhead-1 up front, then kt-2+kAhead by the
+    // wait for slice kt-1
+    const int last = kt == 0 ? min(kAhead - 1, nk - 1) : min(kt + kAhead - 2, nk - 1);
+    const int issued_after = last - kt;
+    // compiler-level fences: s_barrier alone does not keep LDS reads from
+    // being moved across it (no hardware wait is emitted for these)
+    asm volatile("" ::: "memory");
+    if (issued_after >= 3) wait_cnt<3 * PER_STAGE, 0>();
+    else if (issued_after == 2) wait_cnt<2 * PER_STAGE, 0>();
+    else if (issued_after == 1) wait_cnt<PER_STAGE, 0>();
+    else wait_cnt<0, 0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  auto mfma_step = [&](f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM], const bf16x8 (&fb)[TN]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
 
   for (int it = 0;; ++it) {
-    const int u = it * G + slot;
-    if (u >= total) break;
-    // super-rows of kGroupM m-tiles; inside one, m-tile fastest
-    const int sr = u / (kGroupM * n_nt);
-    const int rem = u - sr * (kGroupM * n_nt);
-    const int gm = min(kGroupM, n_mt - sr * kGroupM);
-    const int nt = rem / gm;
-    const int2 te = g.tiles[sr * kGroupM + rem % gm];
-    const int32_t *gr = g.groups + 4 * te.x;
-    const int e = gr[1], row0 = gr[2], n = gr[3];
-    const int m0 = te.y * BM;
-    const int rows_valid = min(BM, n - m0);
-    const int n0 = nt * BN;
-    const int cols_valid = min(BN, g.N - n0);
-    const uint16_t *Ab = g.A + int64_t(row0 + m0) * g.lda;
-    const uint16_t *Bb = g.B + int64_t(e) * g.b_expert_stride + int64_t(n0) * g.Kdim;
-
-    int64_t a_off[A_CH], b_off[B_CH];
-    int a_lds[A_CH], b_lds[B_CH];
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) {
-      const int c = tid + i * NT, r = c >> 3, kc = c & 7;
-      a_off[i] = int64_t(min(r, rows_valid - 1)) * g.lda + kc * 8;
-      a_lds[i] = lds_swz(r, kc);
-    }
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) {
-      const int c = tid + i * NT, r = c >> 3, kc = c & 7;
-      b_off[i] = int64_t(min(r, cols_valid - 1)) * g.Kdim + kc * 8;
-      b_lds[i] = lds_swz(r, kc);
-    }
-
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -169,92 +301,81 @@ __global__ __launch_bounds__(64 * WAVES_M *WAVES_N) void gemm_bf16_kernel(GemmAr
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
-
-    i32x4 ra[A_CH], rb[B_CH];
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const i32x4 *>(Ab + a_off[i]);
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) rb[i] = *reinterpret_cast<const i32x4 *>(Bb + b_off[i]);
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) *reinterpret_cast<i32x4 *>(&sA[0][a_lds[i]]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) *reinterpret_cast<i32x4 *>(&sB[0][b_lds[i]]) = rb[i];
+    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+    wait_slice(0);
+    read_frags(0, 0, fa0, fb0);
+    // the last slice is peeled so the loop body has no branch around the LDS
+    // reads (the wait inserted at such a join would drain the fresh reads)
+    for (int kt = 0; kt < nk - 1; ++kt) {
+      read_frags(kt, 1, fa1, fb1);
+      mfma_step(acc, fa0, fb0);
+      // slice kt+kAhead reuses the buffer of slice kt, whose second half was
+      // read just above (the wait drains those reads)
+      wait_slice(kt + 1);
+      if (kt + kAhead < nk) issue(kt + kAhead);
+      read_frags(kt + 1, 0, fa0, fb0);
+      mfma_step(acc, fa1, fb1);
+    }
+    read_frags(nk - 1, 1, fa1, fb1);
+    mfma_step(acc, fa0, fb0);
+    mfma_step(acc, fa1, fb1);
+    // every wave is done with the ring before the next tile's slices land
     __syncthreads();
-
-    for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt & 1;
-      const bool more = kt + 1 < nk;
-      if (more) {
-        const int64_t k0 = int64_t(kt + 1) * kBK;
-#pragma unroll
-        for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const i32x4 *>(Ab + a_off[i] + k0);
-#pragma unroll
-        for (int i = 0; i < B_CH; ++i) rb[i] = *reinterpret_cast<const i32x4 *>(Bb + b_off[i] + k0);
-      }
-#pragma unroll
-      for (int ks = 0; ks < kBK / 16; ++ks) {
-        const int kc = ks * 2 + (lane >> 5);
-        bf16x8 af[TM], bfr[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const int r = wm * WM + i * 32 + (lane & 31);
-          af[i] = *reinterpret_cast<const bf16x8 *>(&sA[cur][lds_swz(r, kc)]);
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int r = wn * WN + j * 32 + (lane & 31);
-          bfr[j] = *reinterpret_cast<const bf16x8 *>(&sB[cur][lds_swz(r, kc)]);
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-      }
-      if (more) {
-#pragma unroll
-        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<i32x4 *>(&sA[cur ^ 1][a_lds[i]]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < B_CH; ++i) *reinterpret_cast<i32x4 *>(&sB[cur ^ 1][b_lds[i]]) = rb[i];
-      }
-      __syncthreads();
+    const TileCoord c = t;
+    const bool more = decode_tile<BM, BN>(g, (it + 1) * G + slot, n_mt, n_nt, t);
+    if (more) {
+      setup(t);
+      prologue();
     }
 
-    // epilogue. Accumulator slot q of lane l in a 32x32 block holds
-    // row 8*(q/4) + 4*(l/32) + q%4, column l%32.
-    uint16_t *Cb = g.C + int64_t(row0 + m0) * g.ldc;
+    // Epilogue. Accumulator slot q of lane l in a 32x32 block holds row
+    // 8 (q / 4) + 4 (l / 32) + q % 4 and column l % 32 of the block. Rows are
+    // split into a per-lane part (rows_left, lane_off) and a compile-time part,
+    // so nothing per (i, q) stays live across tiles; the asm keeps the
+    // per-tile values from being hoisted out of the tile loop.
+    int32_t ldc_b = int32_t(g.ldc) * 2;
+    int32_t rows_left = c.rows_valid - (wm * WM + 4 * (lane >> 5));
+    asm volatile("" : "+s"(ldc_b), "+v"(rows_left));
+    char *Cc = reinterpret_cast<char *>(g.C + int64_t(c.row0 + c.m0 + wm * WM) * g.ldc) +
+               int64_t(4 * (lane >> 5)) * ldc_b;
+    __builtin_amdgcn_sched_barrier(0);
     if (kSwiglu) {
 #pragma unroll
       for (int p = 0; p < TN / 2; ++p) {
-        const int pc = n0 + wn * WN + p * 64;  // packed column of this gate block
+        const int pc = c.n0 + wn * WN + p * 64;
         if (pc >= g.N) continue;
         const int f = (pc / 64) * 32 + (lane & 31);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int q = 0; q < 16; ++q) {
-            const int r = wm * WM + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-            if (r < rows_valid) {
+            const int rq = i * 32 + 8 * (q >> 2) + (q & 3);
+            if (rq < rows_left) {
               const float gv = acc[i][2 * p][q], uv = acc[i][2 * p + 1][q];
-              const float act = gv / (1.0f + __expf(-gv)) * uv;
-              Cb[int64_t(r) * g.ldc + f] = f32_to_bf16(act);
+              *reinterpret_cast<uint16_t *>(Cc + (int64_t(rq) * ldc_b + f * 2)) =
+                  f32_to_bf16(gv / (1.0f + __expf(-gv)) * uv);
             }
+            if ((q & 3) == 3) __builtin_amdgcn_sched_barrier(0);
           }
       }
     } else {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn * WN + j * 32 + (lane & 31);
-        if (col >= g.N) continue;
+        const int col = c.n0 + wn * WN + j * 32 + (lane & 31);
+        if (c.n0 + wn * WN + j * 32 >= g.N) continue;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int q = 0; q < 16; ++q) {
-            const int r = wm * WM + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-            if (r < rows_valid) Cb[int64_t(r) * g.ldc + col] = f32_to_bf16(acc[i][j][q]);
+            const int rq = i * 32 + 8 * (q >> 2) + (q & 3);
+            if (rq < rows_left)
+              *reinterpret_cast<uint16_t *>(Cc + (int64_t(rq) * ldc_b + col * 2)) =
+                  f32_to_bf16(acc[i][j][q]);
+            if ((q & 3) == 3) __builtin_amdgcn_sched_barrier(0);
           }
       }
     }
+    if (!more) break;
   }
 }
 
@@ -343,10 +464,10 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
   int32_t *n_mtiles = reinterpret_cast<int32_t *>(ws);
   int2 *tiles = reinterpret_cast<int2 *>(ws + L.tiles_off);
   void *act = ws + L.act_off;
-  const int grid = ((cu_count() * 2) + 7) / 8 * 8;
   if (a.dtype == LLEP_BF16) {
+    const int grid = (cu_count() + 7) / 8 * 8;  // one workgroup per CU, XCD-balanced
     hipLaunchKernelGGL(tile_table_kernel, dim3(1), dim3(256), 0, stream, a.groups, a.group_begin,
-                       a.device, a.P, kBM, tiles, n_mtiles);
+                       a.device, a.P, kTileM, tiles, n_mtiles);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g1;
@@ -361,8 +482,7 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g1.n_mtiles = n_mtiles;
     g1.N = 2 * a.F;
     g1.Kdim = a.D;
-    hipLaunchKernelGGL((gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, true>), dim3(grid),
-                       dim3(64 * kWavesM * kWavesN), 0, stream, g1);
+    hipLaunchKernelGGL((gemm256_kernel<256, true>), dim3(grid), dim3(256), 0, stream, g1);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g2 = g1;
@@ -374,8 +494,11 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g2.ldc = a.D;
     g2.N = a.D;
     g2.Kdim = a.F;
-    hipLaunchKernelGGL((gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, false>), dim3(grid),
-                       dim3(64 * kWavesM * kWavesN), 0, stream, g2);
+    // the down projection's N is D: 192-wide tiles divide D = 2880 exactly
+    if (a.D % 256 != 0 && a.D % 192 == 0)
+      hipLaunchKernelGGL((gemm256_kernel<192, false>), dim3(grid), dim3(256), 0, stream, g2);
+    else
+      hipLaunchKernelGGL((gemm256_kernel<256, false>), dim3(grid), dim3(256), 0, stream, g2);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(ffn_f32_gate_up_kernel, dim3(1024), dim3(256), 0, stream,
