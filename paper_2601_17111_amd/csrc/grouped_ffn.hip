@@ -26,6 +26,12 @@
 namespace llep {
 
 constexpr int kTileM = 256;  // rows per GEMM tile (one m-tile never spans two groups)
+#ifndef LLEP_GEMM_WAVES
+#define LLEP_GEMM_WAVES 8
+#endif
+// wave layout of a 256 x 256 tile (and of the 256 x 192 down-projection tile)
+constexpr int kWavesM = 2, kWavesN = LLEP_GEMM_WAVES / 2;
+constexpr int kWavesM192 = LLEP_GEMM_WAVES / 2, kWavesN192 = 2;
 #ifndef LLEP_GROUP_M
 #define LLEP_GROUP_M 8
 #endif
@@ -141,11 +147,22 @@ constexpr int kAhead = LLEP_AHEAD;     // slices requested ahead
 // DMA completions are in issue order, so the compiler's own vmcnt waits for
 // other loads stay correct (they can only wait longer).
 __device__ __forceinline__ void dma16(const char *src, uint16_t *lds_block) {
-  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_ptr)(lds_block)));
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(lds), "v"(src)
-               : "memory", "m0");
+  // wave-uniform by construction; readfirstlane lets the compiler keep it in
+  // an SGPR for the s_mov to m0
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_ptr)(lds_block))));
+  // m0 is reserved to the compiler: saved and restored inside the asm
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_nop 0\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(src)
+      : "memory");
 }
 
 // s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited on)
@@ -189,16 +206,21 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, 
   return true;
 }
 
-template <int BN, bool kSwiglu>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <int BN, int WAVES_M, int WAVES_N, bool kSwiglu>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
+__attribute__((amdgpu_waves_per_eu(WAVES_M * WAVES_N / 4, WAVES_M * WAVES_N / 4)))
 void gemm256_kernel(GemmArgs g) {
   constexpr int BM = 256;
-  constexpr int WM = 128, WN = BN / 2;
+  constexpr int NW = WAVES_M * WAVES_N;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int A_BLK = BM / 16 / 4;  // DMA instructions per wave per stage
-  constexpr int B_BLK = BN / 16 / 4;
-  constexpr int PER_STAGE = A_BLK + B_BLK;
-  static_assert((BN / 16) % 4 == 0, "BN");
+  // DMA blocks (16 rows each) per stage, dealt round-robin over the waves;
+  // every wave issues at least MIN_PER_WAVE of them per stage
+  constexpr int A_BLOCKS = BM / 16, B_BLOCKS = BN / 16;
+  constexpr int BLOCKS = A_BLOCKS + B_BLOCKS;
+  constexpr int MAX_PER_WAVE = (BLOCKS + NW - 1) / NW;
+  constexpr int PER_STAGE = BLOCKS / NW;  // MIN_PER_WAVE: waits count this many
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
   static_assert(kAhead <= kStages && kAhead <= 4, "ring");
   static_assert(!kSwiglu || (WN % 64) == 0, "SwiGLU needs gate/up column pairs per wave");
   __shared__ __attribute__((aligned(1024))) uint16_t sA[kStages][BM * kSK];
@@ -206,7 +228,7 @@ void gemm256_kernel(GemmArgs g) {
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int n_mt = *g.n_mtiles;
   const int n_nt = (g.N + BN - 1) / BN;
   const int G = gridDim.x;  // a multiple of 8
@@ -218,29 +240,34 @@ void gemm256_kernel(GemmArgs g) {
   TileCoord t;
   if (!decode_tile<BM, BN>(g, slot, n_mt, n_nt, t)) return;
   const char *Ab, *Bb;
-  int32_t a_off[A_BLK], b_off[B_BLK];
+  int32_t off[MAX_PER_WAVE];
   auto setup = [&](const TileCoord &c) {
     Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
     Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
          int64_t(c.n0) * ldb_b;
 #pragma unroll
-    for (int j = 0; j < A_BLK; ++j) {
-      const int r = min((wave * A_BLK + j) * 16 + (lane >> 2), c.rows_valid - 1);
-      a_off[j] = int32_t(r * lda_b + kc_load * 16);
-    }
-#pragma unroll
-    for (int j = 0; j < B_BLK; ++j) {
-      const int r = min((wave * B_BLK + j) * 16 + (lane >> 2), c.cols_valid - 1);
-      b_off[j] = int32_t(r * ldb_b + kc_load * 16);
+    for (int j = 0; j < MAX_PER_WAVE; ++j) {
+      const int b = wave + NW * j;
+      if (b < A_BLOCKS) {
+        const int r = min(b * 16 + (lane >> 2), c.rows_valid - 1);
+        off[j] = int32_t(r * lda_b + kc_load * 16);
+      } else {
+        const int r = min((b - A_BLOCKS) * 16 + (lane >> 2), c.cols_valid - 1);
+        off[j] = int32_t(r * ldb_b + kc_load * 16);
+      }
     }
   };
   auto issue = [&](int kt) {
     const int st = kt % kStages;
     const int kb = kt * kSK * 2;
 #pragma unroll
-    for (int j = 0; j < A_BLK; ++j) dma16(Ab + a_off[j] + kb, &sA[st][(wave * A_BLK + j) * 512]);
-#pragma unroll
-    for (int j = 0; j < B_BLK; ++j) dma16(Bb + b_off[j] + kb, &sB[st][(wave * B_BLK + j) * 512]);
+    for (int j = 0; j < MAX_PER_WAVE; ++j) {
+      const int b = wave + NW * j;
+      if (b < A_BLOCKS)
+        dma16(Ab + off[j] + kb, &sA[st][b * 512]);
+      else if (b < BLOCKS)
+        dma16(Bb + off[j] + kb, &sB[st][(b - A_BLOCKS) * 512]);
+    }
   };
   auto prologue = [&]() {
 #pragma unroll
@@ -482,7 +509,9 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g1.n_mtiles = n_mtiles;
     g1.N = 2 * a.F;
     g1.Kdim = a.D;
-    hipLaunchKernelGGL((gemm256_kernel<256, true>), dim3(grid), dim3(256), 0, stream, g1);
+    constexpr int NT = 64 * kWavesM * kWavesN;
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, true>), dim3(grid), dim3(NT), 0,
+                       stream, g1);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g2 = g1;
@@ -496,9 +525,11 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g2.Kdim = a.F;
     // the down projection's N is D: 192-wide tiles divide D = 2880 exactly
     if (a.D % 256 != 0 && a.D % 192 == 0)
-      hipLaunchKernelGGL((gemm256_kernel<192, false>), dim3(grid), dim3(256), 0, stream, g2);
+      hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, false>), dim3(grid),
+                         dim3(64 * kWavesM192 * kWavesN192), 0, stream, g2);
     else
-      hipLaunchKernelGGL((gemm256_kernel<256, false>), dim3(grid), dim3(256), 0, stream, g2);
+      hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, false>), dim3(grid), dim3(NT), 0,
+                         stream, g2);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(ffn_f32_gate_up_kernel, dim3(1024), dim3(256), 0, stream,
