@@ -45,6 +45,10 @@ def _parse():
     ap.add_argument("--cpu-sample-rows", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ep", action="store_true", help="skip the standard-EP comparison")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before warmup, run a plain 1 GiB -> 1 GiB elementwise copy (torch.neg on "
+                         "float32) three times: a kernel of known traffic that scales the HBM "
+                         "counters of a rocprofv3 --pmc run of this command")
     return ap.parse_args()
 
 
@@ -194,6 +198,14 @@ def main():
     torch.cuda.synchronize()
     n_rows = dev_rows[dstar]
 
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+
     for _ in range(args.warmup):
         layer.plan(run["ids"])
         layer.permute(run["ids"], run["gates"], run["x"])
@@ -232,7 +244,7 @@ def main():
         "roofline": {
             "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": tflops / PEAK_BF16_TFLOPS, "traffic": traffic,
-            "kernel": "llep_grouped_ffn on the most-loaded device (gemm_bf16_kernel x2 + tile list)",
+            "kernel": "llep_grouped_ffn on the most-loaded device (tile_table_kernel + gemm256_kernel x2)",
             "flops_per_launch": flops,
         },
         "segments_ms": seg,
