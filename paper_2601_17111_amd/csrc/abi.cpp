@@ -125,6 +125,7 @@ int llep_permute(const llep_plan_params *params, const llep_plan_buffers *plan,
   a.R = params->T * params->K;
   a.K = params->K;
   a.E = params->E;
+  a.max_chunks = 2 * params->E + params->P;
   a.D = D;
   a.n_tiles = int32_t(llep::rank_tiles(a.R));
   a.elem_bytes = elem_bytes(dtype);

@@ -9,12 +9,6 @@
 namespace llep {
 
 constexpr int kWave = 64;
-// Pairs are ranked in tiles of kRankTile pairs; each of the kRankWaves waves
-// of a tile owns a contiguous kRankSub-pair slice of it.
-constexpr int kRankTile = 4096;
-constexpr int kRankWaves = 4;
-constexpr int kRankSub = kRankTile / kRankWaves;
-
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));

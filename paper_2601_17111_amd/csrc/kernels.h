@@ -14,6 +14,14 @@ constexpr int kMaxChunks = 2 * LLEP_MAX_EXPERTS + LLEP_MAX_DEVICES;
 // count is bounded by 2E + P).
 constexpr int32_t kStatusPlanOverflow = 1 << 30;
 
+// Pairs are counted and ranked in tiles of kRankTile pairs (one workgroup
+// each); each of the kRankWaves waves of a tile owns a contiguous
+// kRankSub-pair slice of it. rank_base holds one row of E counts (then
+// exclusive bases) per tile.
+constexpr int kRankTile = 1024;
+constexpr int kRankWaves = 4;
+constexpr int kRankSub = kRankTile / kRankWaves;
+
 int64_t rank_tiles(int64_t R);
 
 struct PlanArgs {
@@ -30,6 +38,7 @@ hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
 struct PermuteArgs {
   int64_t T, R;
   int32_t K, E, D;
+  int32_t max_chunks;  // 2E + P: rows of the plan's chunk table
   int32_t n_tiles;
   int32_t elem_bytes;
   const int32_t *ids;

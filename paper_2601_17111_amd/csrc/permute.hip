@@ -9,8 +9,9 @@
 //                base rank per expert comes from the plan's scan of the
 //                histogram; inside the tile each wave owns a contiguous slice
 //                and ranks its pairs with ballot-built match masks, so the
-//                order never depends on atomics. Writes pair_row, row_pair
-//                and gate_perm.
+//                order never depends on atomics. The chunk table is copied
+//                to LDS first, so finding a pair's chunk reads no memory.
+//                Writes pair_row, row_pair and gate_perm.
 // gather_kernel  one wavefront per token: reads x[t] once (16-byte vectors)
 //                and writes it to the K rows of the token's pairs.
 #include "common.h"
@@ -20,17 +21,31 @@ namespace llep {
 
 __global__ __launch_bounds__(256) void rank_kernel(
     const int32_t *__restrict__ ids, const float *__restrict__ gates, int64_t R,
-    int32_t E, const int32_t *__restrict__ rank_base,
+    int32_t E, int32_t max_chunks, const int32_t *__restrict__ rank_base,
     const int32_t *__restrict__ chunks, const int32_t *__restrict__ chunk_row,
     const int32_t *__restrict__ expert_chunk_begin, int32_t *__restrict__ pair_row,
     int32_t *__restrict__ row_pair, float *__restrict__ gate_perm) {
-  extern __shared__ int32_t wbase[];  // [kRankWaves][E]
+  // LDS: per-wave bases [kRankWaves][E], then the plan's chunk table
+  // (expert_chunk_begin [E+1]; start, end, first row per chunk)
+  extern __shared__ int32_t smem[];
+  int32_t *wbase = smem;
+  int32_t *ecb = wbase + kRankWaves * E;
+  int32_t *c_start = ecb + (E + 1);
+  int32_t *c_end = c_start + kMaxChunks;
+  int32_t *c_row = c_end + kMaxChunks;
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int nb = bits_for(uint32_t(E));
   const int64_t tile0 = int64_t(blockIdx.x) * kRankTile;
   const int64_t s0 = tile0 + int64_t(w) * kRankSub;
+  const int nc = min(max(expert_chunk_begin[E], 0), min(max_chunks, kMaxChunks));
   for (int i = tid; i < kRankWaves * E; i += blockDim.x) wbase[i] = 0;
+  for (int i = tid; i <= E; i += blockDim.x) ecb[i] = min(max(expert_chunk_begin[i], 0), nc);
+  for (int c = tid; c < nc; c += blockDim.x) {
+    c_start[c] = chunks[4 * c + 2];
+    c_end[c] = chunks[4 * c + 3];
+    c_row[c] = chunk_row[c];
+  }
   __syncthreads();
 
   // pass A: per-wave counts of each expert in the wave's slice
@@ -72,13 +87,13 @@ __global__ __launch_bounds__(256) void rank_kernel(
     __builtin_amdgcn_wave_barrier();
     if (e < uint32_t(E) && (m & lanemask_lt()) == 0) wbase[w * E + e] += __popcll(m);
     if (e < uint32_t(E)) {
-      int c = expert_chunk_begin[e];
-      const int c_end = expert_chunk_begin[e + 1];
-      while (c + 1 < c_end && r >= chunks[4 * c + 3]) ++c;
+      int c = ecb[e];
+      const int c1 = max(ecb[e + 1], c);
+      while (c + 1 < c1 && r >= c_end[c]) ++c;
       // a pair outside every chunk of its expert (a plan built from other
       // ids) gets no row
-      const bool inside = c < c_end && r >= chunks[4 * c + 2] && r < chunks[4 * c + 3];
-      const int32_t row = inside ? chunk_row[c] + (r - chunks[4 * c + 2]) : -1;
+      const bool inside = c < c1 && r >= c_start[c] && r < c_end[c];
+      const int32_t row = inside ? c_row[c] + (r - c_start[c]) : -1;
       pair_row[p] = row;
       if (row >= 0 && row < R) {
         row_pair[row] = int32_t(p);
@@ -126,9 +141,9 @@ __global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x
 
 hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
   if (a.R == 0) return hipSuccess;
-  hipLaunchKernelGGL(rank_kernel, dim3(a.n_tiles), dim3(256),
-                     size_t(kRankWaves) * a.E * sizeof(int32_t), stream, a.ids, a.gates,
-                     a.R, a.E, a.plan.rank_base, a.plan.chunks, a.plan.chunk_row,
+  const size_t lds = (size_t(kRankWaves + 1) * a.E + 1 + 3 * size_t(kMaxChunks)) * sizeof(int32_t);
+  hipLaunchKernelGGL(rank_kernel, dim3(a.n_tiles), dim3(256), lds, stream, a.ids, a.gates,
+                     a.R, a.E, a.max_chunks, a.plan.rank_base, a.plan.chunks, a.plan.chunk_row,
                      a.plan.expert_chunk_begin, a.pair_row, a.row_pair, a.gate_perm);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
