@@ -105,10 +105,47 @@ __global__ __launch_bounds__(256) void rank_kernel(
   }
 }
 
-// One wavefront per token; each lane moves 16-byte vectors. kBatch vectors
-// per lane are loaded before they are stored, to keep loads in flight.
-constexpr int kBatch = 4;
+// Access choices, measured on MI355X with the gpt-oss-120b, deepseek-v3 and
+// qwen3-30b layer shapes inside the full step: non-temporal loads of
+// out_perm raise the combine from 0.62-0.65 to 0.73-0.79 of HBM peak;
+// non-temporal loads in the gather gain nothing and non-temporal stores of
+// x_perm lose 10-15%. Four pairs' rows of at most 4 vectors per lane are in
+// flight per combine step (1 or 2 measured within 2%).
+constexpr bool kGatherNtLoad = false;
+constexpr bool kGatherNtStore = false;
+constexpr bool kCombineNtLoad = true;
+constexpr bool kCombineNtStore = false;
+constexpr int kCombinePairs = 4;
+constexpr int kCombineMaxVecs = 4;
+constexpr int kGatherMaxVecs = 8;
 
+template <bool kNT>
+__device__ __forceinline__ i32x4 stream_load(const i32x4 *p) {
+  if (kNT) return __builtin_nontemporal_load(p);
+  return *p;
+}
+template <bool kNT>
+__device__ __forceinline__ void stream_store(i32x4 *p, const i32x4 &v) {
+  if (kNT)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
+}
+
+// Vectors per lane per pass for a row of `vecs` 16-byte vectors: the fewest
+// passes of at most max_per_lane vectors, split evenly (a row of 2880 bf16 =
+// 360 vectors is one pass of 6 per lane, or two of 3).
+inline int vecs_per_lane(int32_t vecs, int max_per_lane) {
+  const int vpl = (vecs + kWave - 1) / kWave;
+  const int passes = (vpl + max_per_lane - 1) / max_per_lane;
+  return (vpl + passes - 1) / passes;
+}
+
+// One wavefront per (token, slice of kV * 64 vectors of its row): the slice
+// is loaded once (all kV vectors per lane in flight) and stored to the rows
+// of the token's K pairs. Row indices come in as one vector load per 64 pairs and are read
+// back with v_readlane, so the stores need no further memory round trip.
+template <int kV>
 __global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x,
                                                      i32x4 *__restrict__ x_perm,
                                                      const int32_t *__restrict__ pair_row,
@@ -116,27 +153,42 @@ __global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x
                                                      int64_t R) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = lane_id();
-  for (int64_t t = int64_t(blockIdx.x) * 4 + w; t < T; t += int64_t(gridDim.x) * 4) {
+  const int nslices = (vecs + kV * kWave - 1) / (kV * kWave);
+  for (int64_t wid = int64_t(blockIdx.x) * 4 + w; wid < T * nslices;
+       wid += int64_t(gridDim.x) * 4) {
+    const int64_t t = wid / nslices;
     const i32x4 *src = x + t * vecs;
-    for (int v0 = 0; v0 < vecs; v0 += kBatch * kWave) {
-      i32x4 val[kBatch];
+    {
+      const int v0 = int(wid % nslices) * kV * kWave;
+      i32x4 val[kV];
 #pragma unroll
-      for (int b = 0; b < kBatch; ++b) {
+      for (int b = 0; b < kV; ++b) {
         const int v = v0 + b * kWave + lane;
-        if (v < vecs) val[b] = src[v];
+        if (v < vecs) val[b] = stream_load<kGatherNtLoad>(src + v);
       }
-      for (int k = 0; k < K; ++k) {
-        const int32_t row = pair_row[t * K + k];
-        if (row < 0 || row >= R) continue;
-        i32x4 *dst = x_perm + int64_t(row) * vecs;
+      for (int kb = 0; kb < K; kb += kWave) {
+        const int nk = min(kWave, K - kb);
+        const int32_t rv = lane < nk ? pair_row[t * K + kb + lane] : -1;
+        for (int k = 0; k < nk; ++k) {
+          const int32_t row = __builtin_amdgcn_readlane(rv, k);
+          if (row < 0 || row >= R) continue;
+          i32x4 *dst = x_perm + int64_t(row) * vecs;
 #pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
-          const int v = v0 + b * kWave + lane;
-          if (v < vecs) dst[v] = val[b];
+          for (int b = 0; b < kV; ++b) {
+            const int v = v0 + b * kWave + lane;
+            if (v < vecs) stream_store<kGatherNtStore>(dst + v, val[b]);
+          }
         }
       }
     }
   }
+}
+
+template <int kV>
+void launch_gather_v(int grid, hipStream_t stream, const PermuteArgs &a, int32_t vecs) {
+  hipLaunchKernelGGL(gather_kernel<kV>, dim3(grid), dim3(256), 0, stream,
+                     static_cast<const i32x4 *>(a.x), static_cast<i32x4 *>(a.x_perm),
+                     a.pair_row, a.T, a.K, vecs, a.R);
 }
 
 hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
@@ -148,11 +200,19 @@ hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int32_t vecs = int32_t((int64_t(a.D) * a.elem_bytes) / 16);
-  const int64_t blocks = (a.T + 3) / 4;
+  const int kv = vecs_per_lane(vecs, kGatherMaxVecs);
+  const int64_t blocks = (a.T * ((vecs + kv * kWave - 1) / (kv * kWave)) + 3) / 4;
   const int grid = int(blocks < 65536 ? blocks : 65536);
-  hipLaunchKernelGGL(gather_kernel, dim3(grid), dim3(256), 0, stream,
-                     static_cast<const i32x4 *>(a.x), static_cast<i32x4 *>(a.x_perm),
-                     a.pair_row, a.T, a.K, vecs, a.R);
+  switch (kv) {
+    case 1: launch_gather_v<1>(grid, stream, a, vecs); break;
+    case 2: launch_gather_v<2>(grid, stream, a, vecs); break;
+    case 3: launch_gather_v<3>(grid, stream, a, vecs); break;
+    case 4: launch_gather_v<4>(grid, stream, a, vecs); break;
+    case 5: launch_gather_v<5>(grid, stream, a, vecs); break;
+    case 6: launch_gather_v<6>(grid, stream, a, vecs); break;
+    case 7: launch_gather_v<7>(grid, stream, a, vecs); break;
+    default: launch_gather_v<8>(grid, stream, a, vecs); break;
+  }
   return hipGetLastError();
 }
 
@@ -161,7 +221,11 @@ hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
 // k ascending, float32 accumulation, one rounding to the output type.
 // ---------------------------------------------------------------------------
 
-template <bool kBf16>
+// One wavefront per (token, slice of kV * 64 vectors of the output row);
+// the pairs' rows are read kCombinePairs at a time with all their loads in
+// flight before they are summed (in k order, so the result does not depend
+// on the slicing).
+template <bool kBf16, int kV>
 __global__ __launch_bounds__(256) void combine_kernel(const i32x4 *__restrict__ out_perm,
                                                       const int32_t *__restrict__ pair_row,
                                                       const float *__restrict__ gates,
@@ -169,42 +233,69 @@ __global__ __launch_bounds__(256) void combine_kernel(const i32x4 *__restrict__ 
                                                       int32_t K, int32_t vecs) {
   const int64_t R = T * K;
   constexpr int kElems = kBf16 ? 8 : 4;
+  constexpr int kPairs = kCombinePairs;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = lane_id();
-  for (int64_t t = int64_t(blockIdx.x) * 4 + w; t < T; t += int64_t(gridDim.x) * 4) {
-    for (int v0 = 0; v0 < vecs; v0 += kBatch * kWave) {
-      float acc[kBatch][kElems];
+  const int nslices = (vecs + kV * kWave - 1) / (kV * kWave);
+  for (int64_t wid = int64_t(blockIdx.x) * 4 + w; wid < T * nslices;
+       wid += int64_t(gridDim.x) * 4) {
+    const int64_t t = wid / nslices;
+    {
+      const int v0 = int(wid % nslices) * kV * kWave;
+      float acc[kV][kElems];
 #pragma unroll
-      for (int b = 0; b < kBatch; ++b)
+      for (int b = 0; b < kV; ++b)
 #pragma unroll
         for (int i = 0; i < kElems; ++i) acc[b][i] = 0.0f;
-      for (int k = 0; k < K; ++k) {
-        const int32_t row = pair_row[t * K + k];
-        if (row < 0 || row >= R) continue;
-        const float g = gates[t * K + k];
-        const i32x4 *src = out_perm + int64_t(row) * vecs;
+      for (int kb = 0; kb < K; kb += kWave) {
+        const int nk = min(kWave, K - kb);
+        int32_t rv = lane < nk ? pair_row[t * K + kb + lane] : -1;
+        if (rv >= R) rv = -1;
+        const float gv = lane < nk ? gates[t * K + kb + lane] : 0.0f;
+        for (int k0 = 0; k0 < nk; k0 += kPairs) {
+          int32_t row[kPairs];
+          float g[kPairs];
+          i32x4 q[kPairs][kV];
 #pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
-          const int v = v0 + b * kWave + lane;
-          if (v < vecs) {
-            const i32x4 q = src[v];
-            if (kBf16) {
+          for (int j = 0; j < kPairs; ++j) {
+            row[j] = k0 + j < nk ? __builtin_amdgcn_readlane(rv, k0 + j) : -1;
+            g[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gv), k0 + j < nk ? k0 + j : 0));
+          }
 #pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const uint32_t u = uint32_t(q[i]);
-                acc[b][2 * i] = fmaf(g, __uint_as_float(u << 16), acc[b][2 * i]);
-                acc[b][2 * i + 1] = fmaf(g, __uint_as_float(u & 0xffff0000u), acc[b][2 * i + 1]);
+          for (int j = 0; j < kPairs; ++j) {
+            if (row[j] < 0) continue;
+            const i32x4 *src = out_perm + int64_t(row[j]) * vecs;
+#pragma unroll
+            for (int b = 0; b < kV; ++b) {
+              const int v = v0 + b * kWave + lane;
+              if (v < vecs) q[j][b] = stream_load<kCombineNtLoad>(src + v);
+            }
+          }
+#pragma unroll
+          for (int j = 0; j < kPairs; ++j) {
+            if (row[j] < 0) continue;
+#pragma unroll
+            for (int b = 0; b < kV; ++b) {
+              const int v = v0 + b * kWave + lane;
+              if (v >= vecs) continue;
+              if (kBf16) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                  const uint32_t u = uint32_t(q[j][b][i]);
+                  acc[b][2 * i] = fmaf(g[j], __uint_as_float(u << 16), acc[b][2 * i]);
+                  acc[b][2 * i + 1] = fmaf(g[j], __uint_as_float(u & 0xffff0000u), acc[b][2 * i + 1]);
+                }
+              } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[b][i] = fmaf(g[j], __int_as_float(q[j][b][i]), acc[b][i]);
               }
-            } else {
-#pragma unroll
-              for (int i = 0; i < 4; ++i) acc[b][i] = fmaf(g, __int_as_float(q[i]), acc[b][i]);
             }
           }
         }
       }
       i32x4 *dst = y + t * vecs;
 #pragma unroll
-      for (int b = 0; b < kBatch; ++b) {
+      for (int b = 0; b < kV; ++b) {
         const int v = v0 + b * kWave + lane;
         if (v < vecs) {
           i32x4 q;
@@ -217,10 +308,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const i32x4 *__restrict__ 
 #pragma unroll
             for (int i = 0; i < 4; ++i) q[i] = __float_as_int(acc[b][i]);
           }
-          dst[v] = q;
+          stream_store<kCombineNtStore>(dst + v, q);
         }
       }
     }
+  }
+}
+
+template <bool kBf16, int kV>
+void launch_combine_v(int grid, hipStream_t stream, const CombineArgs &a, int32_t vecs) {
+  hipLaunchKernelGGL((combine_kernel<kBf16, kV>), dim3(grid), dim3(256), 0, stream,
+                     static_cast<const i32x4 *>(a.out_perm), a.pair_row, a.gates,
+                     static_cast<i32x4 *>(a.y), a.T, a.K, vecs);
+}
+
+template <bool kBf16>
+void launch_combine_t(hipStream_t stream, const CombineArgs &a, int32_t vecs) {
+  const int kv = vecs_per_lane(vecs, kCombineMaxVecs);
+  const int64_t blocks = (a.T * ((vecs + kv * kWave - 1) / (kv * kWave)) + 3) / 4;
+  const int grid = int(blocks < 65536 ? blocks : 65536);
+  switch (kv) {
+    case 1: launch_combine_v<kBf16, 1>(grid, stream, a, vecs); break;
+    case 2: launch_combine_v<kBf16, 2>(grid, stream, a, vecs); break;
+    case 3: launch_combine_v<kBf16, 3>(grid, stream, a, vecs); break;
+    default: launch_combine_v<kBf16, 4>(grid, stream, a, vecs); break;
   }
 }
 
@@ -228,16 +339,10 @@ hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;
   const int eb = a.dtype == LLEP_BF16 ? 2 : 4;
   const int32_t vecs = int32_t((int64_t(a.D) * eb) / 16);
-  const int64_t blocks = (a.T + 3) / 4;
-  const int grid = int(blocks < 65536 ? blocks : 65536);
   if (a.dtype == LLEP_BF16)
-    hipLaunchKernelGGL(combine_kernel<true>, dim3(grid), dim3(256), 0, stream,
-                       static_cast<const i32x4 *>(a.out_perm), a.pair_row, a.gates,
-                       static_cast<i32x4 *>(a.y), a.T, a.K, vecs);
+    launch_combine_t<true>(stream, a, vecs);
   else
-    hipLaunchKernelGGL(combine_kernel<false>, dim3(grid), dim3(256), 0, stream,
-                       static_cast<const i32x4 *>(a.out_perm), a.pair_row, a.gates,
-                       static_cast<i32x4 *>(a.y), a.T, a.K, vecs);
+    launch_combine_t<false>(stream, a, vecs);
   return hipGetLastError();
 }
 

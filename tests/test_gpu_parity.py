@@ -82,6 +82,45 @@ def test_plan_random_matches_oracle(dev, case):
     assert_plan_equal(got, info, ref)
 
 
+def _tight_cases():
+    """Many experts (several 64-expert blocks of the greedy loop), capacities
+    below and above the balanced load, several spilling experts per block,
+    experts whose native device is already over capacity (Case 3), and
+    force-assigns (m > 1 or P * cap < R)."""
+    rng = np.random.default_rng(777)
+    cases = []
+    shapes = [(96, 2), (96, 8), (192, 8), (192, 32), (320, 4), (320, 64), (512, 16), (512, 64)]
+    for i in range(24):
+        E, P = shapes[i % len(shapes)]
+        T, K = int(rng.integers(500, 4000)), int(rng.choice([1, 4, 8]))
+        kind = i % 3
+        if kind == 0:    # zipf over a shuffled expert order
+            w = (np.arange(E) + 1.0) ** -float(rng.uniform(0.8, 1.6))
+            ids = rng.choice(E, size=(T, K), p=rng.permutation(w / w.sum()))
+        elif kind == 1:  # a hot block of experts on a few devices
+            hot = rng.choice(E, size=max(1, E // 16), replace=False)
+            ids = np.where(rng.random((T, K)) < 0.7, rng.choice(hot, size=(T, K)),
+                           rng.integers(0, E, (T, K)))
+        else:            # experts of device 0 all heavy: Case 3 for some of them
+            M = E // P
+            ids = np.where(rng.random((T, K)) < 0.6, rng.integers(0, M, (T, K)),
+                           rng.integers(0, E, (T, K)))
+        R = T * K
+        cap = max(1, int(math.ceil(R / P) * [0.5, 0.9, 1.0, 1.3][i % 4]))
+        m = [1, 5, 50][i % 3]
+        cases.append((ids.astype(np.int32), E, P, cap, m))
+    return cases
+
+
+@pytest.mark.parametrize("case", _tight_cases(),
+                         ids=lambda c: f"E{c[1]}P{c[2]}R{c[0].size}cap{c[3]}m{c[4]}")
+def test_plan_tight_capacity_matches_oracle(dev, case):
+    ids, E, P, cap, m = case
+    got, info, _ = run_plan(ids, E, P, cap, m, dev=dev)
+    ref = oracle.plan(ids.reshape(-1).tolist(), E, P, cap, m)
+    assert_plan_equal(got, info, ref)
+
+
 @pytest.mark.parametrize("E,P", [(512, 64), (512, 8), (256, 64)])
 def test_plan_max_sizes(dev, E, P):
     rng = np.random.default_rng(E + P)
