@@ -131,26 +131,19 @@ struct GemmArgs {
 typedef __attribute__((address_space(3))) void *lds_void_ptr;
 typedef __attribute__((address_space(1))) void *gbl_void_ptr;
 
-#ifndef LLEP_STAGES
-#define LLEP_STAGES 4
-#endif
-#ifndef LLEP_AHEAD
-#define LLEP_AHEAD 4
-#endif
-constexpr int kSK = 32;                // k-slice per LDS stage
-constexpr int kStages = LLEP_STAGES;   // LDS ring
-constexpr int kAhead = LLEP_AHEAD;     // slices requested ahead
+constexpr int kSK = 32;      // k-slice per LDS stage
+constexpr int kAhead = 4;    // slices requested ahead of the one being read
+// One stage more than the look-ahead: slice kt+kAhead is requested before
+// the barrier that releases slice kt+1, into the buffer of slice kt-1 (free
+// since the previous barrier), so after a barrier the MFMAs restart at once.
+constexpr int kStages = kAhead + 1;
 
 // The DMA is issued through asm so the compiler does not treat it as a
 // pending LDS write: it would otherwise wait for every DMA in flight before
 // each LDS read. The kernel orders DMA and reads itself (wait_cnt + barrier);
 // DMA completions are in issue order, so the compiler's own vmcnt waits for
 // other loads stay correct (they can only wait longer).
-__device__ __forceinline__ void dma16(const char *src, uint16_t *lds_block) {
-  // wave-uniform by construction; readfirstlane lets the compiler keep it in
-  // an SGPR for the s_mov to m0
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_ptr)(lds_block))));
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds) {
   // m0 is reserved to the compiler: saved and restored inside the asm
   uint32_t saved;
   asm volatile(
@@ -165,6 +158,12 @@ __device__ __forceinline__ void dma16(const char *src, uint16_t *lds_block) {
       : "memory");
 }
 
+// LDS byte address of a shared-memory object (wave-uniform; once per kernel)
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_ptr)(p))));
+}
+
 // s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited on)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -177,6 +176,18 @@ template <int VM, int LGKM>
 __device__ __forceinline__ void wait_cnt() {
   static_assert(VM >= 0 && VM < 64 && LGKM >= 0 && LGKM < 16, "waitcnt");
   __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | 0x70 | (LGKM << 8));
+}
+
+// Wait until at most VM of this wave's DMA instructions are in flight and
+// its LDS reads are done, then meet the other waves. The compiler-level
+// fences keep LDS reads from being moved across the barrier (s_barrier alone
+// does not order them, and no hardware wait is emitted for DMA targets).
+template <int VM>
+__device__ __forceinline__ void wait_and_sync() {
+  asm volatile("" ::: "memory");
+  wait_cnt<VM, 0>();
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 __device__ __forceinline__ int lds_swz32(int row, int kc) {
@@ -214,14 +225,19 @@ void gemm256_kernel(GemmArgs g) {
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 32, TN = WN / 32;
-  // DMA blocks (16 rows each) per stage, dealt round-robin over the waves;
-  // every wave issues at least MIN_PER_WAVE of them per stage
+  // DMA blocks (16 rows each) per stage, dealt round-robin over the waves:
+  // every wave has A_PER_WAVE A blocks and B_FULL B blocks, the first B_REM
+  // waves one B block more. Waits count the PER_STAGE instructions every
+  // wave issues per slice (conservative for the waves with one more).
   constexpr int A_BLOCKS = BM / 16, B_BLOCKS = BN / 16;
-  constexpr int BLOCKS = A_BLOCKS + B_BLOCKS;
-  constexpr int MAX_PER_WAVE = (BLOCKS + NW - 1) / NW;
-  constexpr int PER_STAGE = BLOCKS / NW;  // MIN_PER_WAVE: waits count this many
+  constexpr int A_PER_WAVE = A_BLOCKS / NW;
+  constexpr int B_FULL = B_BLOCKS / NW, B_REM = B_BLOCKS % NW;
+  constexpr int B_SLOTS = B_FULL + (B_REM ? 1 : 0);
+  constexpr int PER_STAGE = A_PER_WAVE + B_FULL;
+  constexpr uint32_t A_STAGE_BYTES = BM * kSK * 2, B_STAGE_BYTES = BN * kSK * 2;
+  static_assert(A_BLOCKS % NW == 0 && PER_STAGE > 0, "DMA split");
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
-  static_assert(kAhead <= kStages && kAhead <= 4, "ring");
+  static_assert(kAhead == 4, "waits below are written for four slices ahead");
   static_assert(!kSwiglu || (WN % 64) == 0, "SwiGLU needs gate/up column pairs per wave");
   __shared__ __attribute__((aligned(1024))) uint16_t sA[kStages][BM * kSK];
   __shared__ __attribute__((aligned(1024))) uint16_t sB[kStages][BN * kSK];
@@ -236,43 +252,42 @@ void gemm256_kernel(GemmArgs g) {
   const int nk = g.Kdim / kSK;
   const int kc_load = (lane & 3) ^ ((lane >> 4) & 3);
   const int64_t lda_b = g.lda * 2, ldb_b = int64_t(g.Kdim) * 2;
+  const uint32_t sA0 = lds_addr(&sA[0][0]), sB0 = lds_addr(&sB[0][0]);
 
   TileCoord t;
   if (!decode_tile<BM, BN>(g, slot, n_mt, n_nt, t)) return;
   const char *Ab, *Bb;
-  int32_t off[MAX_PER_WAVE];
+  int32_t offA[A_PER_WAVE], offB[B_SLOTS];
   auto setup = [&](const TileCoord &c) {
     Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
     Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
          int64_t(c.n0) * ldb_b;
+    // rows past the tile's valid rows re-read its last valid row (in bounds)
 #pragma unroll
-    for (int j = 0; j < MAX_PER_WAVE; ++j) {
-      const int b = wave + NW * j;
-      if (b < A_BLOCKS) {
-        const int r = min(b * 16 + (lane >> 2), c.rows_valid - 1);
-        off[j] = int32_t(r * lda_b + kc_load * 16);
-      } else {
-        const int r = min((b - A_BLOCKS) * 16 + (lane >> 2), c.cols_valid - 1);
-        off[j] = int32_t(r * ldb_b + kc_load * 16);
-      }
+    for (int j = 0; j < A_PER_WAVE; ++j) {
+      const int r = min((wave + NW * j) * 16 + (lane >> 2), c.rows_valid - 1);
+      offA[j] = int32_t(r * lda_b + kc_load * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < B_SLOTS; ++j) {
+      const int r = min((wave + NW * j) * 16 + (lane >> 2), c.cols_valid - 1);
+      offB[j] = int32_t(r * ldb_b + kc_load * 16);
     }
   };
-  auto issue = [&](int kt) {
-    const int st = kt % kStages;
-    const int kb = kt * kSK * 2;
+  // request the slice at byte offset kb along K into stage st
+  auto issue = [&](int st, int kb) {
+    const uint32_t a_st = sA0 + st * A_STAGE_BYTES, b_st = sB0 + st * B_STAGE_BYTES;
 #pragma unroll
-    for (int j = 0; j < MAX_PER_WAVE; ++j) {
-      const int b = wave + NW * j;
-      if (b < A_BLOCKS)
-        dma16(Ab + off[j] + kb, &sA[st][b * 512]);
-      else if (b < BLOCKS)
-        dma16(Bb + off[j] + kb, &sB[st][(b - A_BLOCKS) * 512]);
-    }
+    for (int j = 0; j < A_PER_WAVE; ++j) dma16(Ab + offA[j] + kb, a_st + (wave + NW * j) * 1024);
+#pragma unroll
+    for (int j = 0; j < B_FULL; ++j) dma16(Bb + offB[j] + kb, b_st + (wave + NW * j) * 1024);
+    if (B_REM != 0 && wave < B_REM)
+      dma16(Bb + offB[B_SLOTS - 1] + kb, b_st + (wave + NW * B_FULL) * 1024);
   };
   auto prologue = [&]() {
 #pragma unroll
     for (int k = 0; k < kAhead; ++k)
-      if (k < nk) issue(k);
+      if (k < nk) issue(k, k * kSK * 2);
   };
   setup(t);
   prologue();
@@ -280,11 +295,11 @@ void gemm256_kernel(GemmArgs g) {
   // MFMA operands of one 16-deep k-step: TM (A) and TN (B) 16-byte
   // fragments per lane. Two sets alternate: the set for the next k-step is
   // read from LDS while the current one feeds the MFMAs, so LDS latency hides
-  // behind 16 MFMAs.
+  // behind the MFMAs.
   static_assert(kSK == 32, "two k-steps per slice");
-  auto read_frags = [&](int kt, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
-    const uint16_t *a_s = sA[kt % kStages];
-    const uint16_t *b_s = sB[kt % kStages];
+  auto read_frags = [&](int st, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
+    const uint16_t *a_s = sA[st];
+    const uint16_t *b_s = sB[st];
     const int kc = ks * 2 + (lane >> 5);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -293,32 +308,14 @@ void gemm256_kernel(GemmArgs g) {
     for (int j = 0; j < TN; ++j)
       fb[j] = *reinterpret_cast<const bf16x8 *>(&b_s[lds_swz32(wn * WN + j * 32 + (lane & 31), kc)]);
   };
-  // Wait until slice kt is in LDS for every wave; slices requested after it
-  // may stay in flight. Each wave also finishes its own LDS reads first, so
-  // after the barrier the buffer of slice kt-1 (in registers everywhere) can
-  // be refilled.
-  auto wait_slice = [&](int kt) {
-    // requested so far: 0 .. kAhead-1 up front, then kt-2+kAhead by the
-    // wait for slice kt-1
-    const int last = kt == 0 ? min(kAhead - 1, nk - 1) : min(kt + kAhead - 2, nk - 1);
-    const int issued_after = last - kt;
-    // compiler-level fences: s_barrier alone does not keep LDS reads from
-    // being moved across it (no hardware wait is emitted for these)
-    asm volatile("" ::: "memory");
-    if (issued_after >= 3) wait_cnt<3 * PER_STAGE, 0>();
-    else if (issued_after == 2) wait_cnt<2 * PER_STAGE, 0>();
-    else if (issued_after == 1) wait_cnt<PER_STAGE, 0>();
-    else wait_cnt<0, 0>();
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-  };
   auto mfma_step = [&](f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM], const bf16x8 (&fb)[TN]) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
   };
+  auto next_stage = [](int st) { return st + 1 == kStages ? 0 : st + 1; };
 
   for (int it = 0;; ++it) {
     f32x16 acc[TM][TN];
@@ -329,21 +326,47 @@ void gemm256_kernel(GemmArgs g) {
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
     bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-    wait_slice(0);
-    read_frags(0, 0, fa0, fb0);
-    // the last slice is peeled so the loop body has no branch around the LDS
-    // reads (the wait inserted at such a join would drain the fresh reads)
-    for (int kt = 0; kt < nk - 1; ++kt) {
-      read_frags(kt, 1, fa1, fb1);
+    // slice kt sits in stage kt % kStages; st tracks the slice being read,
+    // st_req the stage of slice kt + kAhead
+    int st = 0, st_req = kAhead % kStages, kb_req = kAhead * kSK * 2;
+    // slices 0 .. min(kAhead, nk) - 1 were requested; wait for slice 0
+    if (nk >= kAhead)
+      wait_and_sync<(kAhead - 1) * PER_STAGE>();
+    else
+      wait_and_sync<0>();
+    read_frags(st, 0, fa0, fb0);
+    int kt = 0;
+    // steady state: request slice kt + kAhead, three slices stay in flight
+    // past slice kt + 1 (compile-time wait count). The last slice is peeled
+    // so no branch joins around the LDS reads (the wait inserted at such a
+    // join would drain the fresh reads).
+    for (; kt < nk - kAhead; ++kt) {
+      read_frags(st, 1, fa1, fb1);
       mfma_step(acc, fa0, fb0);
-      // slice kt+kAhead reuses the buffer of slice kt, whose second half was
-      // read just above (the wait drains those reads)
-      wait_slice(kt + 1);
-      if (kt + kAhead < nk) issue(kt + kAhead);
-      read_frags(kt + 1, 0, fa0, fb0);
+      issue(st_req, kb_req);
+      st_req = next_stage(st_req);
+      kb_req += kSK * 2;
+      wait_and_sync<(kAhead - 1) * PER_STAGE>();
+      st = next_stage(st);
+      read_frags(st, 0, fa0, fb0);
       mfma_step(acc, fa1, fb1);
     }
-    read_frags(nk - 1, 1, fa1, fb1);
+    // tail: everything is requested; nk - 2 - kt slices remain past kt + 1
+    for (; kt < nk - 1; ++kt) {
+      read_frags(st, 1, fa1, fb1);
+      mfma_step(acc, fa0, fb0);
+      const int left = nk - 2 - kt;
+      if (left >= 2)
+        wait_and_sync<2 * PER_STAGE>();
+      else if (left == 1)
+        wait_and_sync<PER_STAGE>();
+      else
+        wait_and_sync<0>();
+      st = next_stage(st);
+      read_frags(st, 0, fa0, fb0);
+      mfma_step(acc, fa1, fb1);
+    }
+    read_frags(st, 1, fa1, fb1);
     mfma_step(acc, fa0, fb0);
     mfma_step(acc, fa1, fb1);
     // every wave is done with the ring before the next tile's slices land
@@ -355,51 +378,60 @@ void gemm256_kernel(GemmArgs g) {
       prologue();
     }
 
-    // Epilogue. Accumulator slot q of lane l in a 32x32 block holds row
-    // 8 (q / 4) + 4 (l / 32) + q % 4 and column l % 32 of the block. Rows are
-    // split into a per-lane part (rows_left, lane_off) and a compile-time part,
-    // so nothing per (i, q) stays live across tiles; the asm keeps the
-    // per-tile values from being hoisted out of the tile loop.
-    int32_t ldc_b = int32_t(g.ldc) * 2;
-    int32_t rows_left = c.rows_valid - (wm * WM + 4 * (lane >> 5));
-    asm volatile("" : "+s"(ldc_b), "+v"(rows_left));
-    char *Cc = reinterpret_cast<char *>(g.C + int64_t(c.row0 + c.m0 + wm * WM) * g.ldc) +
-               int64_t(4 * (lane >> 5)) * ldc_b;
+    // Epilogue. The MFMAs take the weight fragment as their first operand,
+    // so a 32x32 accumulator block is the transposed output block: lane l
+    // holds output row l % 32 and, in slots 4g .. 4g+3, the four consecutive
+    // columns 8g + 4 (l / 32) + 0..3. Each lane therefore stores 8-byte runs
+    // of one row, with one row bound per block.
+    const int32_t ldc_b = int32_t(g.ldc) * 2;
+    int32_t rows_left = c.rows_valid - (wm * WM + (lane & 31));
+    asm volatile("" : "+v"(rows_left));
+    char *Cc = reinterpret_cast<char *>(g.C + int64_t(c.row0 + c.m0 + wm * WM + (lane & 31)) * g.ldc) +
+               8 * (lane >> 5);
     __builtin_amdgcn_sched_barrier(0);
+    auto pack2 = [](float lo, float hi) {
+      return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
+    };
     if (kSwiglu) {
+      // gate columns 64p .. 64p+31 and the matching up columns 64p+32 ..
+      // 64p+63 of the tile give activation columns f = 32 (pc / 64) + 0..31
 #pragma unroll
       for (int p = 0; p < TN / 2; ++p) {
         const int pc = c.n0 + wn * WN + p * 64;
         if (pc >= g.N) continue;
-        const int f = (pc / 64) * 32 + (lane & 31);
+        const int f0 = (pc / 64) * 32;
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+          if (i * 32 >= rows_left) continue;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const int rq = i * 32 + 8 * (q >> 2) + (q & 3);
-            if (rq < rows_left) {
-              const float gv = acc[i][2 * p][q], uv = acc[i][2 * p + 1][q];
-              *reinterpret_cast<uint16_t *>(Cc + (int64_t(rq) * ldc_b + f * 2)) =
-                  f32_to_bf16(gv / (1.0f + __expf(-gv)) * uv);
+          for (int gq = 0; gq < 4; ++gq) {
+            float h[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float gv = acc[i][2 * p][4 * gq + e], uv = acc[i][2 * p + 1][4 * gq + e];
+              h[e] = gv * __builtin_amdgcn_rcpf(1.0f + __expf(-gv)) * uv;
             }
-            if ((q & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+            *reinterpret_cast<uint2 *>(Cc + int64_t(i * 32) * ldc_b + (f0 + 8 * gq) * 2) =
+                make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
           }
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     } else {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        const int col = c.n0 + wn * WN + j * 32 + (lane & 31);
-        if (c.n0 + wn * WN + j * 32 >= g.N) continue;
+        const int n0 = c.n0 + wn * WN + j * 32;
+        if (n0 >= g.N) continue;
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+          if (i * 32 >= rows_left) continue;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const int rq = i * 32 + 8 * (q >> 2) + (q & 3);
-            if (rq < rows_left)
-              *reinterpret_cast<uint16_t *>(Cc + (int64_t(rq) * ldc_b + col * 2)) =
-                  f32_to_bf16(acc[i][j][q]);
-            if ((q & 3) == 3) __builtin_amdgcn_sched_barrier(0);
-          }
+          for (int gq = 0; gq < 4; ++gq)
+            *reinterpret_cast<uint2 *>(Cc + int64_t(i * 32) * ldc_b + (n0 + 8 * gq) * 2) =
+                make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
+                           pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
     if (!more) break;
