@@ -164,11 +164,14 @@ int llep_permute(const llep_plan_params *params, const llep_plan_buffers *plan,
 /* Packed expert weights (untimed setup, once per set of weights).
  * Inputs, as in the paper (FFN(u) = u^T W):
  *   w_gate, w_up [E][D][F], w_down [E][F][D], in `dtype`.
- * Outputs, in `dtype`:
- *   w_gate_up_packed [E][2F][D]: row 64j + c      = column 32j + c of w_gate,
- *                                row 64j + 32 + c = column 32j + c of w_up
- *                                (j < F/32, c < 32), contraction dim last;
- *   w_down_packed    [E][D][F]:  w_down transposed, contraction dim last.
+ * Outputs, in `dtype`, per expert a matrix P[n][k] (n: output column of
+ * the GEMM, k: contraction index, K its length) stored in blocks of 16 rows
+ * x 32 k: element (n, k) at ((n/16) * (K/32) + k/32) * 512 + (n%16) * 32
+ * + k%32 (so each 16-row, 32-deep piece is one contiguous run):
+ *   w_gate_up_packed [E][2F*D]: K = D; P row 64j + c      = column 32j + c
+ *                               of w_gate, P row 64j + 32 + c = column
+ *                               32j + c of w_up (j < F/32, c < 32);
+ *   w_down_packed    [E][D*F]:  K = F; P row d = column d of w_down.
  * Requires D % 64 == 0 and F % 64 == 0.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
 size_t llep_packed_gate_up_bytes(int32_t E, int32_t D, int32_t F,

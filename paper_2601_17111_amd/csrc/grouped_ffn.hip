@@ -44,12 +44,14 @@ struct WsLayout {
 
 static WsLayout ws_layout(int64_t R, int32_t E, int32_t P, int32_t F, llep_dtype dtype) {
   WsLayout L;
-  L.max_mtiles = R / kTileM + (2 * int64_t(E) + P) + 1;
+  const int64_t max_groups = 2 * int64_t(E) + P;
+  L.max_mtiles = R / kTileM + max_groups + 1;
   L.tiles_off = 256;
-  const size_t tiles_bytes = (size_t(L.max_mtiles) * 8 + 255) / 256 * 256;
+  const size_t tiles_bytes = (size_t(L.max_mtiles) * 16 + 255) / 256 * 256;
   L.act_off = L.tiles_off + tiles_bytes;
   const size_t eb = dtype == LLEP_BF16 ? 2 : 4;
-  L.total = L.act_off + size_t(R) * size_t(F) * eb;
+  // each group's activation rows start on a 16-row block boundary
+  L.total = L.act_off + size_t(R + 16 * max_groups) * size_t(F) * eb;
   return L;
 }
 
@@ -58,36 +60,51 @@ size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t F, llep_dtyp
 }
 
 // ---------------------------------------------------------------------------
-// tile list: one entry (group, m-tile) per BM rows of each group of the range
+// tile list: one entry (group, m-tile, padded first row of the group) per BM
+// rows of each group of the range. Padded rows: the groups' rows laid end to
+// end with each group rounded up to a multiple of 16 (the row blocks of the
+// activation matrix).
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void tile_table_kernel(const int32_t *__restrict__ groups,
                                                          const int32_t *__restrict__ group_begin,
                                                          int32_t device, int32_t P, int32_t BM,
-                                                         int2 *__restrict__ tiles,
+                                                         int4 *__restrict__ tiles,
                                                          int32_t *__restrict__ n_tiles) {
-  __shared__ int32_t part[256];
-  __shared__ int32_t run;
+  __shared__ int32_t part[256], prow[256];
+  __shared__ int32_t run, prun;
   const int tid = threadIdx.x;
   const int lo = device < 0 ? group_begin[0] : group_begin[device];
   const int hi = device < 0 ? group_begin[P] : group_begin[device + 1];
-  if (tid == 0) run = 0;
+  if (tid == 0) {
+    run = 0;
+    prun = 0;
+  }
   __syncthreads();
   for (int g0 = lo; g0 < hi; g0 += 256) {
     const int g = g0 + tid;
-    const int mt = g < hi ? (groups[4 * g + 3] + BM - 1) / BM : 0;
+    const int n = g < hi ? groups[4 * g + 3] : 0;
+    const int mt = (n + BM - 1) / BM;
+    const int pr = (n + 15) / 16 * 16;
     part[tid] = mt;
+    prow[tid] = pr;
     __syncthreads();
     for (int off = 1; off < 256; off <<= 1) {
       const int32_t t = tid >= off ? part[tid - off] : 0;
+      const int32_t u = tid >= off ? prow[tid - off] : 0;
       __syncthreads();
       part[tid] += t;
+      prow[tid] += u;
       __syncthreads();
     }
     const int32_t base = run + part[tid] - mt;
-    for (int i = 0; i < mt; ++i) tiles[base + i] = make_int2(g, i);
+    const int32_t pbase = prun + prow[tid] - pr;
+    for (int i = 0; i < mt; ++i) tiles[base + i] = make_int4(g, i, pbase, 0);
     __syncthreads();
-    if (tid == 255) run += part[255];
+    if (tid == 255) {
+      run += part[255];
+      prun += prow[255];
+    }
     __syncthreads();
   }
   if (tid == 0) *n_tiles = run;
@@ -105,7 +122,7 @@ struct GemmArgs {
   uint16_t *C;
   int64_t ldc;
   const int32_t *groups;
-  const int2 *tiles;
+  const int4 *tiles;
   const int32_t *n_mtiles;
   int32_t N, Kdim;
 };
@@ -195,7 +212,7 @@ __device__ __forceinline__ int lds_swz32(int row, int kc) {
 }
 
 struct TileCoord {
-  int e, row0, m0, rows_valid, n0, cols_valid;
+  int e, row0, prow0, m0, rows_valid, n0, cols_valid;
 };
 
 template <int BM, int BN>
@@ -206,10 +223,11 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, 
   const int rem = u - sr * (kGroupM * n_nt);
   const int gm = min(kGroupM, n_mt - sr * kGroupM);
   const int nt = rem / gm;
-  const int2 te = g.tiles[sr * kGroupM + rem % gm];
+  const int4 te = g.tiles[sr * kGroupM + rem % gm];
   const int32_t *gr = g.groups + 4 * te.x;
   t.e = gr[1];
   t.row0 = gr[2];
+  t.prow0 = te.z;
   t.m0 = te.y * BM;
   t.rows_valid = min(BM, gr[3] - t.m0);
   t.n0 = nt * BN;
@@ -217,7 +235,9 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, 
   return true;
 }
 
-template <int BN, int WAVES_M, int WAVES_N, bool kSwiglu>
+// A is row-major (lda) or, with kABlocked, in 16 x 32 blocks over padded
+// rows; C likewise with kCBlocked. B is always in 16 x 32 blocks.
+template <int BN, int WAVES_M, int WAVES_N, bool kSwiglu, bool kABlocked, bool kCBlocked>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
 __attribute__((amdgpu_waves_per_eu(WAVES_M * WAVES_N / 4, WAVES_M * WAVES_N / 4)))
 void gemm256_kernel(GemmArgs g) {
@@ -251,7 +271,11 @@ void gemm256_kernel(GemmArgs g) {
   const int slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
   const int nk = g.Kdim / kSK;
   const int kc_load = (lane & 3) ^ ((lane >> 4) & 3);
-  const int64_t lda_b = g.lda * 2, ldb_b = int64_t(g.Kdim) * 2;
+  const int64_t lda_b = g.lda * 2;
+  // a 16 x 32 block is 1 KB; lane l fills LDS bytes 16l .. 16l+15 = row
+  // l / 4, chunk slot l % 4, which holds logical chunk kc_load of that row
+  const int32_t blk_lane = (lane >> 2) * 64 + kc_load * 16;
+  const int64_t blk_row_b = int64_t(nk) * 1024;  // one 16-row block across K
   const uint32_t sA0 = lds_addr(&sA[0][0]), sB0 = lds_addr(&sB[0][0]);
 
   TileCoord t;
@@ -259,35 +283,48 @@ void gemm256_kernel(GemmArgs g) {
   const char *Ab, *Bb;
   int32_t offA[A_PER_WAVE], offB[B_SLOTS];
   auto setup = [&](const TileCoord &c) {
-    Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
-    Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
-         int64_t(c.n0) * ldb_b;
-    // rows past the tile's valid rows re-read its last valid row (in bounds)
+    // rows (columns) past the tile's valid ones re-read its last valid row
+    // (block), so every address stays in bounds
+    if (kABlocked) {
+      Ab = reinterpret_cast<const char *>(g.A) + ((c.prow0 + c.m0) >> 4) * blk_row_b;
 #pragma unroll
-    for (int j = 0; j < A_PER_WAVE; ++j) {
-      const int r = min((wave + NW * j) * 16 + (lane >> 2), c.rows_valid - 1);
-      offA[j] = int32_t(r * lda_b + kc_load * 16);
+      for (int j = 0; j < A_PER_WAVE; ++j) {
+        const int rb = min(wave + NW * j, (c.rows_valid - 1) >> 4);
+        offA[j] = int32_t(rb * blk_row_b + blk_lane);
+      }
+    } else {
+      Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
+#pragma unroll
+      for (int j = 0; j < A_PER_WAVE; ++j) {
+        const int r = min((wave + NW * j) * 16 + (lane >> 2), c.rows_valid - 1);
+        offA[j] = int32_t(r * lda_b + kc_load * 16);
+      }
     }
+    Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
+         (c.n0 >> 4) * blk_row_b;
 #pragma unroll
     for (int j = 0; j < B_SLOTS; ++j) {
-      const int r = min((wave + NW * j) * 16 + (lane >> 2), c.cols_valid - 1);
-      offB[j] = int32_t(r * ldb_b + kc_load * 16);
+      const int nb = min(wave + NW * j, (c.cols_valid - 1) >> 4);
+      offB[j] = int32_t(nb * blk_row_b + blk_lane);
     }
   };
-  // request the slice at byte offset kb along K into stage st
-  auto issue = [&](int st, int kb) {
+  // request slice kt into stage st: 64 B per row along K for a row-major A,
+  // the next 1 KB block for blocked operands
+  auto issue = [&](int st, int kt) {
     const uint32_t a_st = sA0 + st * A_STAGE_BYTES, b_st = sB0 + st * B_STAGE_BYTES;
+    const int kba = kABlocked ? kt * 1024 : kt * kSK * 2;
+    const int kbb = kt * 1024;
 #pragma unroll
-    for (int j = 0; j < A_PER_WAVE; ++j) dma16(Ab + offA[j] + kb, a_st + (wave + NW * j) * 1024);
+    for (int j = 0; j < A_PER_WAVE; ++j) dma16(Ab + offA[j] + kba, a_st + (wave + NW * j) * 1024);
 #pragma unroll
-    for (int j = 0; j < B_FULL; ++j) dma16(Bb + offB[j] + kb, b_st + (wave + NW * j) * 1024);
+    for (int j = 0; j < B_FULL; ++j) dma16(Bb + offB[j] + kbb, b_st + (wave + NW * j) * 1024);
     if (B_REM != 0 && wave < B_REM)
-      dma16(Bb + offB[B_SLOTS - 1] + kb, b_st + (wave + NW * B_FULL) * 1024);
+      dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NW * B_FULL) * 1024);
   };
   auto prologue = [&]() {
 #pragma unroll
     for (int k = 0; k < kAhead; ++k)
-      if (k < nk) issue(k, k * kSK * 2);
+      if (k < nk) issue(k, k);
   };
   setup(t);
   prologue();
@@ -328,7 +365,7 @@ void gemm256_kernel(GemmArgs g) {
     bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
     // slice kt sits in stage kt % kStages; st tracks the slice being read,
     // st_req the stage of slice kt + kAhead
-    int st = 0, st_req = kAhead % kStages, kb_req = kAhead * kSK * 2;
+    int st = 0, st_req = kAhead % kStages, kt_req = kAhead;
     // slices 0 .. min(kAhead, nk) - 1 were requested; wait for slice 0
     if (nk >= kAhead)
       wait_and_sync<(kAhead - 1) * PER_STAGE>();
@@ -343,9 +380,9 @@ void gemm256_kernel(GemmArgs g) {
     for (; kt < nk - kAhead; ++kt) {
       read_frags(st, 1, fa1, fb1);
       mfma_step(acc, fa0, fb0);
-      issue(st_req, kb_req);
+      issue(st_req, kt_req);
       st_req = next_stage(st_req);
-      kb_req += kSK * 2;
+      ++kt_req;
       wait_and_sync<(kAhead - 1) * PER_STAGE>();
       st = next_stage(st);
       read_frags(st, 0, fa0, fb0);
@@ -382,12 +419,21 @@ void gemm256_kernel(GemmArgs g) {
     // so a 32x32 accumulator block is the transposed output block: lane l
     // holds output row l % 32 and, in slots 4g .. 4g+3, the four consecutive
     // columns 8g + 4 (l / 32) + 0..3. Each lane therefore stores 8-byte runs
-    // of one row, with one row bound per block.
-    const int32_t ldc_b = int32_t(g.ldc) * 2;
+    // of one row, with one row bound per block. 32 rows span 64 * ldc bytes
+    // in both layouts; a blocked C puts column c of a row at block c / 32.
+    const int32_t rows32_b = int32_t(g.ldc) * 64;
     int32_t rows_left = c.rows_valid - (wm * WM + (lane & 31));
     asm volatile("" : "+v"(rows_left));
-    char *Cc = reinterpret_cast<char *>(g.C + int64_t(c.row0 + c.m0 + wm * WM + (lane & 31)) * g.ldc) +
-               8 * (lane >> 5);
+    char *Cc;
+    if (kCBlocked) {
+      const int pr = c.prow0 + c.m0 + wm * WM + (lane & 31);
+      Cc = reinterpret_cast<char *>(g.C + (int64_t(pr >> 4) * (g.ldc >> 5) * 512 + (pr & 15) * 32)) +
+           8 * (lane >> 5);
+    } else {
+      Cc = reinterpret_cast<char *>(g.C + int64_t(c.row0 + c.m0 + wm * WM + (lane & 31)) * g.ldc) +
+           8 * (lane >> 5);
+    }
+    auto col_b = [](int col0) { return kCBlocked ? (col0 >> 5) * 1024 + (col0 & 31) * 2 : col0 * 2; };
     __builtin_amdgcn_sched_barrier(0);
     auto pack2 = [](float lo, float hi) {
       return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
@@ -411,7 +457,7 @@ void gemm256_kernel(GemmArgs g) {
               const float gv = acc[i][2 * p][4 * gq + e], uv = acc[i][2 * p + 1][4 * gq + e];
               h[e] = gv * __builtin_amdgcn_rcpf(1.0f + __expf(-gv)) * uv;
             }
-            *reinterpret_cast<uint2 *>(Cc + int64_t(i * 32) * ldc_b + (f0 + 8 * gq) * 2) =
+            *reinterpret_cast<uint2 *>(Cc + i * rows32_b + col_b(f0 + 8 * gq)) =
                 make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
           }
           __builtin_amdgcn_sched_barrier(0);
@@ -427,7 +473,7 @@ void gemm256_kernel(GemmArgs g) {
           if (i * 32 >= rows_left) continue;
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq)
-            *reinterpret_cast<uint2 *>(Cc + int64_t(i * 32) * ldc_b + (n0 + 8 * gq) * 2) =
+            *reinterpret_cast<uint2 *>(Cc + i * rows32_b + col_b(n0 + 8 * gq)) =
                 make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
                            pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
           __builtin_amdgcn_sched_barrier(0);
@@ -436,6 +482,18 @@ void gemm256_kernel(GemmArgs g) {
     }
     if (!more) break;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Packed weights: each expert's matrix W[n][k] (n = output column of the
+// GEMM, k = contraction index; K a multiple of 32) is stored in blocks of
+// 16 rows x 32 k, block (n / 16, k / 32) at position (n / 16) * (K / 32) +
+// k / 32, row-major inside the block. A slice of 32 k of 16 rows is one
+// contiguous 1 KB (bf16) that one DMA instruction moves.
+// ---------------------------------------------------------------------------
+
+__host__ __device__ __forceinline__ int64_t packed_index(int n, int k, int K) {
+  return (int64_t(n >> 4) * (K >> 5) + (k >> 5)) * 512 + (n & 15) * 32 + (k & 31);
 }
 
 // ---------------------------------------------------------------------------
@@ -476,12 +534,11 @@ __global__ __launch_bounds__(256) void ffn_f32_gate_up_kernel(
     const int e = groups[4 * group_of_row(groups, lo, hi, row) + 1];
     const float *xr = x_perm + int64_t(row) * D;
     const int pg = 64 * (f / 32) + (f % 32);
-    const float *wg = wgu + (int64_t(e) * 2 * F + pg) * D;
-    const float *wu = wg + int64_t(32) * D;
+    const float *we = wgu + int64_t(e) * 2 * F * D;
     float gs = 0.0f, us = 0.0f;
     for (int d = 0; d < D; ++d) {
-      gs = fmaf(xr[d], wg[d], gs);
-      us = fmaf(xr[d], wu[d], us);
+      gs = fmaf(xr[d], we[packed_index(pg, d, D)], gs);
+      us = fmaf(xr[d], we[packed_index(pg + 32, d, D)], us);
     }
     act[int64_t(row) * F + f] = gs / (1.0f + expf(-gs)) * us;
   }
@@ -499,9 +556,9 @@ __global__ __launch_bounds__(256) void ffn_f32_down_kernel(
     const int row = row_first + int(u / D), c = int(u % D);
     const int e = groups[4 * group_of_row(groups, lo, hi, row) + 1];
     const float *ar = act + int64_t(row) * F;
-    const float *w = wd + (int64_t(e) * D + c) * F;
+    const float *we = wd + int64_t(e) * D * F;
     float s = 0.0f;
-    for (int f = 0; f < F; ++f) s = fmaf(ar[f], w[f], s);
+    for (int f = 0; f < F; ++f) s = fmaf(ar[f], we[packed_index(c, f, F)], s);
     out[int64_t(row) * D + c] = s;
   }
 }
@@ -521,7 +578,7 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
   const WsLayout L = ws_layout(a.R, a.E, a.P, a.F, a.dtype);
   char *ws = static_cast<char *>(a.ws);
   int32_t *n_mtiles = reinterpret_cast<int32_t *>(ws);
-  int2 *tiles = reinterpret_cast<int2 *>(ws + L.tiles_off);
+  int4 *tiles = reinterpret_cast<int4 *>(ws + L.tiles_off);
   void *act = ws + L.act_off;
   if (a.dtype == LLEP_BF16) {
     const int grid = (cu_count() + 7) / 8 * 8;  // one workgroup per CU, XCD-balanced
@@ -542,8 +599,8 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g1.N = 2 * a.F;
     g1.Kdim = a.D;
     constexpr int NT = 64 * kWavesM * kWavesN;
-    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, true>), dim3(grid), dim3(NT), 0,
-                       stream, g1);
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, true, false, true>), dim3(grid),
+                       dim3(NT), 0, stream, g1);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g2 = g1;
@@ -557,11 +614,11 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g2.Kdim = a.F;
     // the down projection's N is D: 192-wide tiles divide D = 2880 exactly
     if (a.D % 256 != 0 && a.D % 192 == 0)
-      hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, false>), dim3(grid),
-                         dim3(64 * kWavesM192 * kWavesN192), 0, stream, g2);
+      hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, false, true, false>),
+                         dim3(grid), dim3(64 * kWavesM192 * kWavesN192), 0, stream, g2);
     else
-      hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, false>), dim3(grid), dim3(NT), 0,
-                         stream, g2);
+      hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, false, true, false>), dim3(grid),
+                         dim3(NT), 0, stream, g2);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(ffn_f32_gate_up_kernel, dim3(1024), dim3(256), 0, stream,
@@ -580,8 +637,9 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
 // weight packing: tiled transposes (setup, not on the timed path)
 // ---------------------------------------------------------------------------
 
-// dst[b][map(c)][r] = src[b][r][c]; map: 0 identity, 1 gate slot, 2 up slot
-// of the interleaved gate/up layout.
+// dst[b] at packed_index(map(c), r) = src[b][r][c]; map: 0 identity, 1 gate
+// slot, 2 up slot of the interleaved gate/up layout; the contraction index r
+// runs over the `rows` of src.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ src, T *__restrict__ dst,
                                                         int32_t rows, int32_t cols, int64_t sbs,
@@ -598,7 +656,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ sr
     const int c = c0 + i, r = r0 + tx;
     if (c < cols && r < rows) {
       const int drow = mode == 0 ? c : 64 * (c / 32) + (c % 32) + (mode == 2 ? 32 : 0);
-      dst[b * dbs + int64_t(drow) * rows + r] = tile[tx][i];
+      dst[b * dbs + packed_index(drow, r, rows)] = tile[tx][i];
     }
   }
 }

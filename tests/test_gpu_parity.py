@@ -255,6 +255,35 @@ def test_bf16_layer_small(dev, shape):
     assert np.array_equal(run.forward(-1).float().cpu().numpy(), y_llep)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_pack_weights_layout(dev, dtype):
+    """Every packed element sits where the header's block formula puts it."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    E, D, F = 2, 128, 192
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    g = torch.Generator(device="cpu").manual_seed(3)
+    wg, wu = (torch.randn(E, D, F, generator=g).to(tdt) for _ in range(2))
+    wd = torch.randn(E, F, D, generator=g).to(tdt)
+    gu, dn = B.llep_pack_weights(wg.to(dev), wu.to(dev), wd.to(dev))
+    torch.cuda.synchronize()
+    gu, dn = gu.cpu().reshape(E, -1), dn.cpu().reshape(E, -1)
+
+    def idx(n, k, K):
+        return ((n // 16) * (K // 32) + k // 32) * 512 + (n % 16) * 32 + k % 32
+
+    n = np.arange(2 * F)[:, None]
+    k = np.arange(D)[None, :]
+    j, c = n // 64, n % 64
+    col = 32 * j + c % 32
+    for e in range(E):
+        want = torch.where(torch.from_numpy(c < 32), wg[e].T[col[:, 0]], wu[e].T[col[:, 0]])
+        assert torch.equal(gu[e][torch.from_numpy(idx(n, k, D))], want)
+        nd = np.arange(D)[:, None]
+        kf = np.arange(F)[None, :]
+        assert torch.equal(dn[e][torch.from_numpy(idx(nd, kf, F))], wd[e].T)
+
+
 def test_bf16_single_device_launch(dev):
     """llep_grouped_ffn on one device's groups writes exactly that device's rows."""
     import torch
