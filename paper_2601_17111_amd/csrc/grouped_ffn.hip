@@ -354,6 +354,56 @@ void gemm256_kernel(GemmArgs g) {
   };
   auto next_stage = [](int st) { return st + 1 == kStages ? 0 : st + 1; };
 
+  // One k-step of MFMAs with the side work of the loop spread between them
+  // in a fixed order: after MFMA s come side operations [s NS / NM,
+  // (s+1) NS / NM), where side operation q < NR reads fragment q of k-step
+  // ks_next of stage st_next and q >= NR issues DMA q - NR of slice kt_dma.
+  // The scheduling barriers keep that order, so the memory instructions issue
+  // while the MFMAs execute instead of in bursts between them.
+  constexpr int NM = TM * TN, NR = TM + TN, ND = A_PER_WAVE + B_SLOTS;
+  auto side_op = [&](int q, int st_next, int ks_next, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN],
+                     int st_dma, int kt_dma) {
+    if (q < TM) {
+      const uint16_t *a_s = sA[st_next];
+      fa[q] = *reinterpret_cast<const bf16x8 *>(
+          &a_s[lds_swz32(wm * WM + q * 32 + (lane & 31), ks_next * 2 + (lane >> 5))]);
+    } else if (q < NR) {
+      const uint16_t *b_s = sB[st_next];
+      fb[q - TM] = *reinterpret_cast<const bf16x8 *>(
+          &b_s[lds_swz32(wn * WN + (q - TM) * 32 + (lane & 31), ks_next * 2 + (lane >> 5))]);
+    } else {
+      const int d = q - NR;
+      const uint32_t a_st = sA0 + st_dma * A_STAGE_BYTES, b_st = sB0 + st_dma * B_STAGE_BYTES;
+      const int kba = kABlocked ? kt_dma * 1024 : kt_dma * kSK * 2;
+      const int kbb = kt_dma * 1024;
+      if (d < A_PER_WAVE)
+        dma16(Ab + offA[d] + kba, a_st + (wave + NW * d) * 1024);
+      else if (d < A_PER_WAVE + B_FULL)
+        dma16(Bb + offB[d - A_PER_WAVE] + kbb, b_st + (wave + NW * (d - A_PER_WAVE)) * 1024);
+      else if (wave < B_REM)
+        dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NW * B_FULL) * 1024);
+    }
+  };
+  auto interleaved_step = [&](f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM],
+                              const bf16x8 (&fb)[TN], bf16x8 (&fa_next)[TM],
+                              bf16x8 (&fb_next)[TN], int st_next, int ks_next, bool with_dma,
+                              int st_dma, int kt_dma) {
+    const int NS = NR + (with_dma ? ND : 0);
+#pragma unroll
+    for (int s = 0; s < NM; ++s) {
+      acc[s / TN][s % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          fb[s % TN], fa[s / TN], acc[s / TN][s % TN], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < NR + ND; ++q) {
+        if (q < NS && q * NM >= s * NS && q * NM < (s + 1) * NS) {
+          side_op(q, st_next, ks_next, fa_next, fb_next, st_dma, kt_dma);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  };
+
   for (int it = 0;; ++it) {
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -378,15 +428,14 @@ void gemm256_kernel(GemmArgs g) {
     // so no branch joins around the LDS reads (the wait inserted at such a
     // join would drain the fresh reads).
     for (; kt < nk - kAhead; ++kt) {
-      read_frags(st, 1, fa1, fb1);
-      mfma_step(acc, fa0, fb0);
-      issue(st_req, kt_req);
+      // k-step 0 of slice kt; reads of its k-step 1; DMA of slice kt + kAhead
+      interleaved_step(acc, fa0, fb0, fa1, fb1, st, 1, true, st_req, kt_req);
       st_req = next_stage(st_req);
       ++kt_req;
       wait_and_sync<(kAhead - 1) * PER_STAGE>();
       st = next_stage(st);
-      read_frags(st, 0, fa0, fb0);
-      mfma_step(acc, fa1, fb1);
+      // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1
+      interleaved_step(acc, fa1, fb1, fa0, fb0, st, 0, false, 0, 0);
     }
     // tail: everything is requested; nk - 2 - kt slices remain past kt + 1
     for (; kt < nk - 1; ++kt) {
