@@ -259,8 +259,14 @@ void gemm256_kernel(GemmArgs g) {
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
   static_assert(kAhead == 4, "waits below are written for four slices ahead");
   static_assert(!kSwiglu || (WN % 64) == 0, "SwiGLU needs gate/up column pairs per wave");
-  __shared__ __attribute__((aligned(1024))) uint16_t sA[kStages][BM * kSK];
-  __shared__ __attribute__((aligned(1024))) uint16_t sB[kStages][BN * kSK];
+  // stage s: A rows at s * STAGE_BYTES, then B rows; the last two stages are
+  // also the epilogue's staging area
+  constexpr uint32_t STAGE_BYTES = A_STAGE_BYTES + B_STAGE_BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE_BYTES];
+  auto stageA = [&](int st) { return reinterpret_cast<const uint16_t *>(smem + st * STAGE_BYTES); };
+  auto stageB = [&](int st) {
+    return reinterpret_cast<const uint16_t *>(smem + st * STAGE_BYTES + A_STAGE_BYTES);
+  };
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -276,7 +282,7 @@ void gemm256_kernel(GemmArgs g) {
   // l / 4, chunk slot l % 4, which holds logical chunk kc_load of that row
   const int32_t blk_lane = (lane >> 2) * 64 + kc_load * 16;
   const int64_t blk_row_b = int64_t(nk) * 1024;  // one 16-row block across K
-  const uint32_t sA0 = lds_addr(&sA[0][0]), sB0 = lds_addr(&sB[0][0]);
+  const uint32_t sA0 = lds_addr(smem), sB0 = sA0 + A_STAGE_BYTES;
 
   TileCoord t;
   if (!decode_tile<BM, BN>(g, slot, n_mt, n_nt, t)) return;
@@ -311,7 +317,7 @@ void gemm256_kernel(GemmArgs g) {
   // request slice kt into stage st: 64 B per row along K for a row-major A,
   // the next 1 KB block for blocked operands
   auto issue = [&](int st, int kt) {
-    const uint32_t a_st = sA0 + st * A_STAGE_BYTES, b_st = sB0 + st * B_STAGE_BYTES;
+    const uint32_t a_st = sA0 + st * STAGE_BYTES, b_st = sB0 + st * STAGE_BYTES;
     const int kba = kABlocked ? kt * 1024 : kt * kSK * 2;
     const int kbb = kt * 1024;
 #pragma unroll
@@ -335,8 +341,8 @@ void gemm256_kernel(GemmArgs g) {
   // behind the MFMAs.
   static_assert(kSK == 32, "two k-steps per slice");
   auto read_frags = [&](int st, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
-    const uint16_t *a_s = sA[st];
-    const uint16_t *b_s = sB[st];
+    const uint16_t *a_s = stageA(st);
+    const uint16_t *b_s = stageB(st);
     const int kc = ks * 2 + (lane >> 5);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -364,16 +370,16 @@ void gemm256_kernel(GemmArgs g) {
   auto side_op = [&](int q, int st_next, int ks_next, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN],
                      int st_dma, int kt_dma) {
     if (q < TM) {
-      const uint16_t *a_s = sA[st_next];
+      const uint16_t *a_s = stageA(st_next);
       fa[q] = *reinterpret_cast<const bf16x8 *>(
           &a_s[lds_swz32(wm * WM + q * 32 + (lane & 31), ks_next * 2 + (lane >> 5))]);
     } else if (q < NR) {
-      const uint16_t *b_s = sB[st_next];
+      const uint16_t *b_s = stageB(st_next);
       fb[q - TM] = *reinterpret_cast<const bf16x8 *>(
           &b_s[lds_swz32(wn * WN + (q - TM) * 32 + (lane & 31), ks_next * 2 + (lane >> 5))]);
     } else {
       const int d = q - NR;
-      const uint32_t a_st = sA0 + st_dma * A_STAGE_BYTES, b_st = sB0 + st_dma * B_STAGE_BYTES;
+      const uint32_t a_st = sA0 + st_dma * STAGE_BYTES, b_st = sB0 + st_dma * STAGE_BYTES;
       const int kba = kABlocked ? kt_dma * 1024 : kt_dma * kSK * 2;
       const int kbb = kt_dma * 1024;
       if (d < A_PER_WAVE)
@@ -459,75 +465,99 @@ void gemm256_kernel(GemmArgs g) {
     __syncthreads();
     const TileCoord c = t;
     const bool more = decode_tile<BM, BN>(g, (it + 1) * G + slot, n_mt, n_nt, t);
+    // the next tile's first kAhead - 1 slices load during the epilogue; the
+    // last stages hold the epilogue's staging area until the barrier below
+    static_assert(kStages - (kAhead - 1) >= 2, "two stages free for staging");
     if (more) {
       setup(t);
-      prologue();
+#pragma unroll
+      for (int k = 0; k < kAhead - 1; ++k)
+        if (k < nk) issue(k, k);
     }
 
     // Epilogue. The MFMAs take the weight fragment as their first operand,
     // so a 32x32 accumulator block is the transposed output block: lane l
     // holds output row l % 32 and, in slots 4g .. 4g+3, the four consecutive
-    // columns 8g + 4 (l / 32) + 0..3. Each lane therefore stores 8-byte runs
-    // of one row, with one row bound per block. 32 rows span 64 * ldc bytes
-    // in both layouts; a blocked C puts column c of a row at block c / 32.
-    const int32_t rows32_b = int32_t(g.ldc) * 64;
-    int32_t rows_left = c.rows_valid - (wm * WM + (lane & 31));
-    asm volatile("" : "+v"(rows_left));
-    char *Cc;
-    if (kCBlocked) {
-      const int pr = c.prow0 + c.m0 + wm * WM + (lane & 31);
-      Cc = reinterpret_cast<char *>(g.C + (int64_t(pr >> 4) * (g.ldc >> 5) * 512 + (pr & 15) * 32)) +
-           8 * (lane >> 5);
-    } else {
-      Cc = reinterpret_cast<char *>(g.C + int64_t(c.row0 + c.m0 + wm * WM + (lane & 31)) * g.ldc) +
-           8 * (lane >> 5);
-    }
-    auto col_b = [](int col0) { return kCBlocked ? (col0 >> 5) * 1024 + (col0 & 31) * 2 : col0 * 2; };
-    __builtin_amdgcn_sched_barrier(0);
+    // columns 8g + 4 (l / 32) + 0..3. Each wave writes its results to its own
+    // part of the staging area, then reads them back in store order, so the
+    // global stores are contiguous runs: whole 1 KB blocks for a blocked C,
+    // WN-column row segments for a row-major C.
+    constexpr uint32_t STAGING = 2 * STAGE_BYTES / NW;  // bytes per wave
+    char *stg = smem + (kStages - 2) * STAGE_BYTES + wave * STAGING;
+    const int rows_w = c.rows_valid - wm * WM;  // valid rows of this wave's tile part
+    const int h = lane >> 5;
     auto pack2 = [](float lo, float hi) {
       return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
     };
-    if (kSwiglu) {
+    if constexpr (kSwiglu) {
       // gate columns 64p .. 64p+31 and the matching up columns 64p+32 ..
-      // 64p+63 of the tile give activation columns f = 32 (pc / 64) + 0..31
-#pragma unroll
-      for (int p = 0; p < TN / 2; ++p) {
-        const int pc = c.n0 + wn * WN + p * 64;
-        if (pc >= g.N) continue;
-        const int f0 = (pc / 64) * 32;
+      // 64p+63 of the tile give activation columns f = 32 (pc / 64) + 0..31.
+      // One activation block (16 rows x 32 columns, 1 KB) per 16 rows.
+      static_assert(kCBlocked && TN == 2, "SwiGLU writes one 32-column block per wave");
+      static_assert(WM / 16 * 1024 <= STAGING, "staging");
+      const int pc = c.n0 + wn * WN;
+      if (pc < g.N) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-          if (i * 32 >= rows_left) continue;
+          char *blk = stg + (2 * i + ((lane & 31) >> 4)) * 1024 + (lane & 15) * 64;
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
-            float h[4];
+            float hv[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const float gv = acc[i][2 * p][4 * gq + e], uv = acc[i][2 * p + 1][4 * gq + e];
-              h[e] = gv * __builtin_amdgcn_rcpf(1.0f + __expf(-gv)) * uv;
+              const float gv = acc[i][0][4 * gq + e], uv = acc[i][1][4 * gq + e];
+              hv[e] = gv * __builtin_amdgcn_rcpf(1.0f + __expf(-gv)) * uv;
             }
-            *reinterpret_cast<uint2 *>(Cc + i * rows32_b + col_b(f0 + 8 * gq)) =
-                make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
+            *reinterpret_cast<uint2 *>(blk + (8 * gq + 4 * h) * 2) =
+                make_uint2(pack2(hv[0], hv[1]), pack2(hv[2], hv[3]));
           }
-          __builtin_amdgcn_sched_barrier(0);
+        }
+        // block rb of this wave = activation row block (prow0 + m0 + wm WM) / 16 + rb
+        const int64_t rb0 = (c.prow0 + c.m0 + wm * WM) >> 4;
+        char *dst = reinterpret_cast<char *>(g.C) + (rb0 * (g.ldc >> 5) + (pc >> 6)) * 1024 +
+                    lane * 16;
+#pragma unroll
+        for (int rb = 0; rb < WM / 16; ++rb) {
+          if (rb * 16 >= rows_w) break;  // the group's padded rows end here
+          *reinterpret_cast<i32x4 *>(dst + int64_t(rb) * (g.ldc >> 5) * 1024) =
+              *reinterpret_cast<const i32x4 *>(stg + rb * 1024 + lane * 16);
         }
       }
     } else {
+      // row-major C: 32 rows x WN columns per piece, rows RS bytes apart
+      static_assert(!kCBlocked, "blocked C is written by the SwiGLU epilogue only");
+      constexpr int RS = WN * 2;
+      constexpr int CH = WN / 8;  // 16-byte chunks per row segment
+      static_assert(32 * RS <= STAGING, "staging");
+      const int ncol0 = c.n0 + wn * WN;
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n0 = c.n0 + wn * WN + j * 32;
-        if (n0 >= g.N) continue;
+      for (int i = 0; i < TM; ++i) {
+        if (i * 32 >= rows_w) break;
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          if (i * 32 >= rows_left) continue;
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq)
-            *reinterpret_cast<uint2 *>(Cc + i * rows32_b + col_b(n0 + 8 * gq)) =
+            *reinterpret_cast<uint2 *>(stg + (lane & 31) * RS + (j * 32 + 8 * gq + 4 * h) * 2) =
                 make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
                            pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
-          __builtin_amdgcn_sched_barrier(0);
+        char *crow = reinterpret_cast<char *>(
+            g.C + int64_t(c.row0 + c.m0 + wm * WM + i * 32) * g.ldc + ncol0);
+#pragma unroll
+        for (int r0 = 0; r0 < 32 * CH; r0 += kWave) {
+          const int q = r0 + lane;
+          const int row = q / CH, ch = q % CH;
+          if (q < 32 * CH && i * 32 + row < rows_w && ncol0 + ch * 8 < g.N)
+            *reinterpret_cast<i32x4 *>(crow + int64_t(row) * g.ldc * 2 + ch * 16) =
+                *reinterpret_cast<const i32x4 *>(stg + row * RS + ch * 16);
         }
       }
+    }
+    if (more) {
+      // the staging area is the last stages of the ring again: every wave's
+      // staging reads are done (lgkmcnt) before slice kAhead - 1 may land
+      // there; the DMAs and stores in flight are not waited for
+      wait_and_sync<63>();
+      if (kAhead - 1 < nk) issue(kAhead - 1, kAhead - 1);
     }
     if (!more) break;
   }
