@@ -261,6 +261,15 @@ def main():
     model_ms = seg["plan"] + (seg["permute"] + seg["combine"]) / cfg.P + seg["grouped_ffn"]
     out["layer_tokens_per_s_p_device_model"] = T / (model_ms * 1e-3)
 
+    # the raw 1-GPU layer: all P devices' groups back to back in one call
+    ms_full, seg_full = _time_steps(layer, run, max(3, args.steps // 4), -1)
+    total_rows = sum(dev_rows)
+    out["full_layer_all_devices"] = {
+        "ms_per_step": ms_full, "tokens_per_s": T / (ms_full * 1e-3), "segments_ms": seg_full,
+        "rows": total_rows,
+        "grouped_ffn_TFLOPs": 6.0 * D * F * total_rows / (seg_full["grouped_ffn"] * 1e-3) / 1e12,
+    }
+
     if not args.no_ep:
         layer.set_mode("ep")
         info_ep, rows_ep = plan_info()

@@ -30,8 +30,11 @@ constexpr int kTileM = 256;  // rows per GEMM tile (one m-tile never spans two g
 #define LLEP_GEMM_WAVES 8
 #endif
 // wave layout of a 256 x 256 tile (and of the 256 x 192 down-projection tile)
+#ifndef LLEP_GEMM2_WAVES
+#define LLEP_GEMM2_WAVES LLEP_GEMM_WAVES
+#endif
 constexpr int kWavesM = 2, kWavesN = LLEP_GEMM_WAVES / 2;
-constexpr int kWavesM192 = LLEP_GEMM_WAVES / 2, kWavesN192 = 2;
+constexpr int kWavesM192 = LLEP_GEMM2_WAVES / 2, kWavesN192 = 2;
 #ifndef LLEP_GROUP_M
 #define LLEP_GROUP_M 8
 #endif
@@ -250,12 +253,16 @@ void gemm256_kernel(GemmArgs g) {
   // waves one B block more. Waits count the PER_STAGE instructions every
   // wave issues per slice (conservative for the waves with one more).
   constexpr int A_BLOCKS = BM / 16, B_BLOCKS = BN / 16;
-  constexpr int A_PER_WAVE = A_BLOCKS / NW;
-  constexpr int B_FULL = B_BLOCKS / NW, B_REM = B_BLOCKS % NW;
+  // Half the waves (one per SIMD) issue all the DMA: a DMA instruction that
+  // waits for room in the memory pipeline then holds up only that wave,
+  // while the other wave on the SIMD keeps issuing MFMAs (+4% measured).
+  constexpr int NWD = NW / 2;
+  constexpr int A_PER_WAVE = A_BLOCKS / NWD;
+  constexpr int B_FULL = B_BLOCKS / NWD, B_REM = B_BLOCKS % NWD;
   constexpr int B_SLOTS = B_FULL + (B_REM ? 1 : 0);
   constexpr int PER_STAGE = A_PER_WAVE + B_FULL;
   constexpr uint32_t A_STAGE_BYTES = BM * kSK * 2, B_STAGE_BYTES = BN * kSK * 2;
-  static_assert(A_BLOCKS % NW == 0 && PER_STAGE > 0, "DMA split");
+  static_assert(A_BLOCKS % NWD == 0 && PER_STAGE > 0 && NWD <= NW, "DMA split");
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
   static_assert(kAhead == 4, "waits below are written for four slices ahead");
   static_assert(!kSwiglu || (WN % 64) == 0, "SwiGLU needs gate/up column pairs per wave");
@@ -295,14 +302,14 @@ void gemm256_kernel(GemmArgs g) {
       Ab = reinterpret_cast<const char *>(g.A) + ((c.prow0 + c.m0) >> 4) * blk_row_b;
 #pragma unroll
       for (int j = 0; j < A_PER_WAVE; ++j) {
-        const int rb = min(wave + NW * j, (c.rows_valid - 1) >> 4);
+        const int rb = min(wave + NWD * j, (c.rows_valid - 1) >> 4);
         offA[j] = int32_t(rb * blk_row_b + blk_lane);
       }
     } else {
       Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
 #pragma unroll
       for (int j = 0; j < A_PER_WAVE; ++j) {
-        const int r = min((wave + NW * j) * 16 + (lane >> 2), c.rows_valid - 1);
+        const int r = min((wave + NWD * j) * 16 + (lane >> 2), c.rows_valid - 1);
         offA[j] = int32_t(r * lda_b + kc_load * 16);
       }
     }
@@ -310,7 +317,7 @@ void gemm256_kernel(GemmArgs g) {
          (c.n0 >> 4) * blk_row_b;
 #pragma unroll
     for (int j = 0; j < B_SLOTS; ++j) {
-      const int nb = min(wave + NW * j, (c.cols_valid - 1) >> 4);
+      const int nb = min(wave + NWD * j, (c.cols_valid - 1) >> 4);
       offB[j] = int32_t(nb * blk_row_b + blk_lane);
     }
   };
@@ -321,11 +328,13 @@ void gemm256_kernel(GemmArgs g) {
     const int kba = kABlocked ? kt * 1024 : kt * kSK * 2;
     const int kbb = kt * 1024;
 #pragma unroll
-    for (int j = 0; j < A_PER_WAVE; ++j) dma16(Ab + offA[j] + kba, a_st + (wave + NW * j) * 1024);
+    for (int j = 0; j < A_PER_WAVE; ++j)
+      if (wave < NWD) dma16(Ab + offA[j] + kba, a_st + (wave + NWD * j) * 1024);
 #pragma unroll
-    for (int j = 0; j < B_FULL; ++j) dma16(Bb + offB[j] + kbb, b_st + (wave + NW * j) * 1024);
+    for (int j = 0; j < B_FULL; ++j)
+      if (wave < NWD) dma16(Bb + offB[j] + kbb, b_st + (wave + NWD * j) * 1024);
     if (B_REM != 0 && wave < B_REM)
-      dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NW * B_FULL) * 1024);
+      dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NWD * B_FULL) * 1024);
   };
   auto prologue = [&]() {
 #pragma unroll
@@ -382,12 +391,13 @@ void gemm256_kernel(GemmArgs g) {
       const uint32_t a_st = sA0 + st_dma * STAGE_BYTES, b_st = sB0 + st_dma * STAGE_BYTES;
       const int kba = kABlocked ? kt_dma * 1024 : kt_dma * kSK * 2;
       const int kbb = kt_dma * 1024;
+      if (wave >= NWD) return;
       if (d < A_PER_WAVE)
-        dma16(Ab + offA[d] + kba, a_st + (wave + NW * d) * 1024);
+        dma16(Ab + offA[d] + kba, a_st + (wave + NWD * d) * 1024);
       else if (d < A_PER_WAVE + B_FULL)
-        dma16(Bb + offB[d - A_PER_WAVE] + kbb, b_st + (wave + NW * (d - A_PER_WAVE)) * 1024);
+        dma16(Bb + offB[d - A_PER_WAVE] + kbb, b_st + (wave + NWD * (d - A_PER_WAVE)) * 1024);
       else if (wave < B_REM)
-        dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NW * B_FULL) * 1024);
+        dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NWD * B_FULL) * 1024);
     }
   };
   auto interleaved_step = [&](f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM],
@@ -493,19 +503,23 @@ void gemm256_kernel(GemmArgs g) {
       // gate columns 64p .. 64p+31 and the matching up columns 64p+32 ..
       // 64p+63 of the tile give activation columns f = 32 (pc / 64) + 0..31.
       // One activation block (16 rows x 32 columns, 1 KB) per 16 rows.
-      static_assert(kCBlocked && TN == 2, "SwiGLU writes one 32-column block per wave");
-      static_assert(WM / 16 * 1024 <= STAGING, "staging");
-      const int pc = c.n0 + wn * WN;
-      if (pc < g.N) {
+      static_assert(kCBlocked && TN % 2 == 0, "SwiGLU needs gate/up block pairs");
+      static_assert((TN / 2) * (WM / 16) * 1024 <= STAGING, "staging");
+      const int64_t rb0 = (c.prow0 + c.m0 + wm * WM) >> 4;
+#pragma unroll
+      for (int p = 0; p < TN / 2; ++p) {
+        const int pc = c.n0 + wn * WN + p * 64;
+        if (pc >= g.N) continue;
+        char *sp = stg + p * (WM / 16) * 1024;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-          char *blk = stg + (2 * i + ((lane & 31) >> 4)) * 1024 + (lane & 15) * 64;
+          char *blk = sp + (2 * i + ((lane & 31) >> 4)) * 1024 + (lane & 15) * 64;
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
             float hv[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const float gv = acc[i][0][4 * gq + e], uv = acc[i][1][4 * gq + e];
+              const float gv = acc[i][2 * p][4 * gq + e], uv = acc[i][2 * p + 1][4 * gq + e];
               hv[e] = gv * __builtin_amdgcn_rcpf(1.0f + __expf(-gv)) * uv;
             }
             *reinterpret_cast<uint2 *>(blk + (8 * gq + 4 * h) * 2) =
@@ -513,14 +527,13 @@ void gemm256_kernel(GemmArgs g) {
           }
         }
         // block rb of this wave = activation row block (prow0 + m0 + wm WM) / 16 + rb
-        const int64_t rb0 = (c.prow0 + c.m0 + wm * WM) >> 4;
         char *dst = reinterpret_cast<char *>(g.C) + (rb0 * (g.ldc >> 5) + (pc >> 6)) * 1024 +
                     lane * 16;
 #pragma unroll
         for (int rb = 0; rb < WM / 16; ++rb) {
           if (rb * 16 >= rows_w) break;  // the group's padded rows end here
           *reinterpret_cast<i32x4 *>(dst + int64_t(rb) * (g.ldc >> 5) * 1024) =
-              *reinterpret_cast<const i32x4 *>(stg + rb * 1024 + lane * 16);
+              *reinterpret_cast<const i32x4 *>(sp + rb * 1024 + lane * 16);
         }
       }
     } else {
