@@ -49,6 +49,10 @@ def _parse():
                     help="before warmup, run a plain 1 GiB -> 1 GiB elementwise copy (torch.neg on "
                          "float32) three times: a kernel of known traffic that scales the HBM "
                          "counters of a rocprofv3 --pmc run of this command")
+    ap.add_argument("--sweep", choices=["alpha", "lambda", "batch", "all"],
+                    help="instead of the bench line: the planner-knob and batch sweeps of the "
+                         "paper's ablations on the gpt-oss-120b layer shape, one JSON line per "
+                         "point (LLEP vs standard EP, P-device model)")
     return ap.parse_args()
 
 
@@ -160,8 +164,77 @@ def _cpu_baseline(cfg, inp, expert_weights, args):
     }
 
 
+def _sweep(args):
+    """Ablation sweeps (Sec. 5.3 factor alpha, adaptive ratio lambda, batch size)
+    on the gpt-oss-120b layer shape with a hot set of 4 experts: per point the
+    most-loaded device's rows and the P-device model time of LLEP and of
+    standard EP. Communication is not modelled (one GPU)."""
+    import torch
+    from fractions import Fraction
+    from paper_2601_17111_amd import binding as B
+    from paper_2601_17111_amd.layer import LLEPLayer
+    from paper_2601_17111_amd.synth import CONFIGS, make_inputs, make_weights
+
+    B.lib()
+    dev = "cuda:0"
+    base = CONFIGS["gpt-oss-120b"].with_(lam=1.3, min_chunk=1024, alpha=Fraction(1))
+    wg, wu, wd = make_weights(base, args.seed, device=dev)
+    gu, dn = B.llep_pack_weights(wg, wu, wd)
+    del wg, wu, wd
+    points = []
+    if args.sweep in ("alpha", "all"):
+        for frac in (0.3, 0.5, 0.8, 0.95):
+            for a in ("1", "3/2", "2", "5/2", "3"):
+                points.append(("alpha", base.with_(routing=("hot", frac, 4), alpha=Fraction(a))))
+    if args.sweep in ("lambda", "all"):
+        for frac in (0.15, 0.2, 0.3, 0.5):
+            for lam in (1.1, 1.4, 1.7, 2.0, 2.3, 2.6):
+                points.append(("lambda", base.with_(T=8192, routing=("hot", frac, 4), lam=lam)))
+    if args.sweep in ("batch", "all"):
+        for frac in (0.3, 0.5, 0.8, 0.95):
+            for T in (4096, 8192, 16384, 32768, 65536):
+                points.append(("batch", base.with_(T=T, routing=("hot", frac, 4))))
+    steps = max(3, args.steps // 4)
+    for kind, cfg in points:
+        inp = make_inputs(cfg, args.seed)
+        run = dict(ids=torch.from_numpy(inp.ids).to(dev), gates=torch.from_numpy(inp.gates).to(dev),
+                   x=torch.from_numpy(inp.x).to(dev).to(torch.bfloat16), gu=gu, dn=dn)
+        res = {}
+        for mode in ("llep", "ep"):
+            layer = LLEPLayer(cfg.T, cfg.K, cfg.E, cfg.P, cfg.D, cfg.F, cfg.capacity, torch.bfloat16,
+                              dev, cfg.min_chunk, cfg.lam, mode)
+            layer.plan(run["ids"])
+            torch.cuda.synchronize()
+            info = layer.bufs.info_dict()
+            d = info["max_device"]
+            rows = layer.bufs.device_rows.cpu().tolist()[d]
+            for _ in range(2):
+                layer.plan(run["ids"]); layer.permute(run["ids"], run["gates"], run["x"])
+                layer.ffn(gu, dn, d); layer.combine(run["gates"])
+            _, seg = _time_steps(layer, run, steps, d)
+            model = seg["plan"] + (seg["permute"] + seg["combine"]) / cfg.P + seg["grouped_ffn"]
+            res[mode] = {"max_device_rows": rows, "bypassed": info["bypassed"],
+                         "forced": info["forced"], "n_xfers": info["n_xfers"],
+                         "segments_ms": seg, "model_ms": model}
+            del layer
+        print(json.dumps({
+            "sweep": kind, "T": cfg.T, "hot_frac": cfg.routing[1], "hot_experts": cfg.routing[2],
+            "alpha": str(cfg.alpha), "lambda": cfg.lam, "min_chunk": cfg.min_chunk,
+            "capacity": cfg.capacity, "llep": res["llep"], "ep": res["ep"],
+            "speedup_model": res["ep"]["model_ms"] / res["llep"]["model_ms"],
+            "speedup_ffn": res["ep"]["segments_ms"]["grouped_ffn"] /
+                           res["llep"]["segments_ms"]["grouped_ffn"],
+        }), flush=True)
+
+
 def main():
     args = _parse()
+    if args.sweep:
+        if args.gpus != 1:
+            print("the sweeps run on one GPU", file=sys.stderr)
+            sys.exit(2)
+        _sweep(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the P devices of the "
               f"plan are virtual devices on that GPU.", file=sys.stderr)

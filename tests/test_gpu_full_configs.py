@@ -72,6 +72,37 @@ def test_full_plan_and_permutation(dev, name, seed):
         assert torch.equal(L.x_perm[rows_t], run.x[src])
 
 
+# the paper's planner settings for its layer benchmarks (lambda = 1.3,
+# alpha = 1, m = 1024) and the alpha / lambda ablation ranges, at full size
+# (hot fraction on 4 experts, alpha, lambda, T, m); the last rows are chosen so
+# the lambda bypass and the force-assign fire
+KNOB_CASES = ([(frac, alpha, lam, T, 1024) for frac in (0.15, 0.3, 0.95)
+               for alpha, lam, T in (("1", 1.3, 32768), ("2", 1.3, 32768), ("5/2", 2.6, 8192))] +
+              [(0.05, "1", 2.6, 8192, 1024), (0.05, "1", 1.3, 8192, 1024),
+               (0.3, "1", 1.3, 32768, 4096), (0.5, "1", 1.3, 8192, 2048)])
+
+
+@pytest.mark.parametrize("frac,alpha,lam,T,m", KNOB_CASES, ids=lambda v: str(v))
+def test_full_plan_paper_knobs(dev, frac, alpha, lam, T, m):
+    """Plans with the min-chunk force-assign (m = 1024) and the lambda bypass
+    active, bit-exact against the oracle; a bypassed plan is the EP plan."""
+    from fractions import Fraction
+    from paper_2601_17111_amd.synth import CONFIGS
+    from gpu_util import run_plan
+    cfg = CONFIGS["gpt-oss-120b"].with_(T=T, routing=("hot", frac, 4), alpha=Fraction(alpha),
+                                        lam=lam, min_chunk=m)
+    from paper_2601_17111_amd.synth import make_inputs
+    ids = make_inputs(cfg, 0, with_x=False).ids
+    got, info, _ = run_plan(ids, cfg.E, cfg.P, cfg.capacity, cfg.min_chunk, lam=cfg.lam, dev=dev)
+    ref = oracle.plan(ids.reshape(-1).tolist(), cfg.E, cfg.P, cfg.capacity, cfg.min_chunk,
+                      lam=cfg.lam)
+    assert_plan_equal(got, info, ref)
+    if ref.bypassed:
+        ep = oracle.plan(ids.reshape(-1).tolist(), cfg.E, cfg.P, cfg.capacity, cfg.min_chunk,
+                         mode="ep")
+        assert ref.chunks == ep.chunks
+
+
 def _expert_subset(cfg, ids, n_extra, rng):
     loads = np.bincount(ids.reshape(-1), minlength=cfg.E)
     order = np.argsort(-loads, kind="stable")
