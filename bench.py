@@ -49,7 +49,7 @@ def _parse():
                     help="before warmup, run a plain 1 GiB -> 1 GiB elementwise copy (torch.neg on "
                          "float32) three times: a kernel of known traffic that scales the HBM "
                          "counters of a rocprofv3 --pmc run of this command")
-    ap.add_argument("--sweep", choices=["alpha", "lambda", "batch", "all"],
+    ap.add_argument("--sweep", choices=["alpha", "lambda", "batch", "all", "experts"],
                     help="instead of the bench line: the planner-knob and batch sweeps of the "
                          "paper's ablations on the gpt-oss-120b layer shape, one JSON line per "
                          "point (LLEP vs standard EP, P-device model)")
@@ -82,6 +82,18 @@ def _traffic(workload):
     if t.get("kernel_hash") != _kernel_hash() or t.get("workload") != workload:
         return None
     return t.get("bytes_per_call")
+
+
+def _m_local_gb(layer, P, D, F, eb):
+    """Peak memory model of each device's share (Sec. 3 cost analysis):
+    sum over the device's groups of (n D + 3 D F + n F) elements, n its rows,
+    3 D F the SwiGLU expert's three weight matrices."""
+    info = layer.bufs.info_dict()
+    groups = layer.bufs.groups[:info["n_groups"]].cpu().tolist()
+    out = [0.0] * P
+    for d, _, _, n in groups:
+        out[d] += (n * D + 3 * D * F + n * F) * eb / 1e9
+    return out
 
 
 def _time_steps(layer, run, steps, dstar):
@@ -227,8 +239,68 @@ def _sweep(args):
         }), flush=True)
 
 
+def _sweep_experts(args):
+    """App. A.1: the same work split evenly over N experts. 65536 tokens, one
+    expert each, D = F = 8192, all experts on one device (P = 1), N in
+    4 .. 256; the grouped SwiGLU FFN over all rows, timed with HIP events.
+    Weights are drawn and packed 16 experts at a time."""
+    import torch
+    from fractions import Fraction
+    from paper_2601_17111_amd import binding as B
+    from paper_2601_17111_amd.layer import LLEPLayer
+    from paper_2601_17111_amd.synth import LayerConfig, make_inputs, make_weights
+
+    B.lib()
+    dev = "cuda:0"
+    T, D, F = 65536, 8192, 8192
+    reps = max(3, args.steps // 4)
+    for N in (4, 16, 32, 64, 128, 256):
+        cfg = LayerConfig(f"a1-n{N}", T=T, D=D, F=F, E=N, K=1, P=1, alpha=Fraction(1),
+                          dtype="bf16", routing=("balanced",))
+        gu = torch.empty((N, 2 * F, D), dtype=torch.bfloat16, device=dev)
+        dn = torch.empty((N, D, F), dtype=torch.bfloat16, device=dev)
+        for b0 in range(0, N, 16):
+            nb = min(16, N - b0)
+            wg, wu, wd = make_weights(cfg.with_(E=nb), args.seed + b0, device=dev)
+            B.llep_pack_weights(wg, wu, wd, out=(gu[b0:b0 + nb], dn[b0:b0 + nb]))
+            del wg, wu, wd
+        inp = make_inputs(cfg, args.seed)
+        ids = torch.from_numpy(inp.ids).to(dev)
+        gates = torch.from_numpy(inp.gates).to(dev)
+        x = torch.from_numpy(inp.x).to(dev).to(torch.bfloat16)
+        layer = LLEPLayer(T, 1, N, 1, D, F, cfg.capacity, torch.bfloat16, dev)
+        layer.plan(ids)
+        layer.permute(ids, gates, x)
+        for _ in range(2):
+            layer.ffn(gu, dn, -1)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            layer.ffn(gu, dn, -1)
+            e.record()
+            torch.cuda.synchronize()
+            ts.append(s.elapsed_time(e))
+        ms = sorted(ts)[len(ts) // 2]
+        flops = 6.0 * D * F * T
+        print(json.dumps({"sweep": "experts", "experts": N, "tokens": T, "D": D, "F": F,
+                          "rows_per_expert": T // N, "grouped_ffn_ms": ms,
+                          "TFLOPs": flops / (ms * 1e-3) / 1e12,
+                          "frac_of_peak": flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}),
+              flush=True)
+        del gu, dn, layer
+        torch.cuda.empty_cache()
+
+
 def main():
     args = _parse()
+    if args.sweep == "experts":
+        if args.gpus != 1:
+            print("the sweeps run on one GPU", file=sys.stderr)
+            sys.exit(2)
+        _sweep_experts(args)
+        return
     if args.sweep:
         if args.gpus != 1:
             print("the sweeps run on one GPU", file=sys.stderr)
@@ -334,6 +406,9 @@ def main():
     model_ms = seg["plan"] + (seg["permute"] + seg["combine"]) / cfg.P + seg["grouped_ffn"]
     out["layer_tokens_per_s_p_device_model"] = T / (model_ms * 1e-3)
 
+    m_llep = _m_local_gb(layer, cfg.P, D, F, eb)
+    out["m_local_GB"] = {"llep_max": max(m_llep), "llep_per_device": m_llep}
+
     # the raw 1-GPU layer: all P devices' groups back to back in one call
     ms_full, seg_full = _time_steps(layer, run, max(3, args.steps // 4), -1)
     total_rows = sum(dev_rows)
@@ -347,6 +422,9 @@ def main():
         layer.set_mode("ep")
         info_ep, rows_ep = plan_info()
         d_ep = info_ep["max_device"]
+        m_ep = _m_local_gb(layer, cfg.P, D, F, eb)
+        out["m_local_GB"].update({"ep_max": max(m_ep), "ep_per_device": m_ep,
+                                  "ep_over_llep": max(m_ep) / max(m_llep)})
         layer.permute(run["ids"], run["gates"], run["x"])
         for _ in range(2):
             layer.ffn(run["gu"], run["dn"], d_ep)

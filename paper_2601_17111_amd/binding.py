@@ -202,13 +202,21 @@ def llep_permute(params: llep_plan_params, bufs: PlanBuffers, topk_ids, topk_gat
                               _stream(stream)), "llep_permute")
 
 
-def llep_pack_weights(w_gate, w_up, w_down, stream=None):
-    """Packed copies of the expert weights (see llep.h); returns (gate_up, down)."""
+def llep_pack_weights(w_gate, w_up, w_down, stream=None, out=None):
+    """Packed copies of the expert weights (see llep.h); returns (gate_up, down).
+    `out` = (gate_up, down) packs into those (contiguous) tensors instead, e.g.
+    slices of a larger packed set filled a few experts at a time."""
     import torch
     E, D, F = w_gate.shape
     code = _dtype_code(w_gate)
-    gu = torch.empty((E, 2 * F, D), dtype=w_gate.dtype, device=w_gate.device)
-    dn = torch.empty((E, D, F), dtype=w_gate.dtype, device=w_gate.device)
+    if out is None:
+        gu = torch.empty((E, 2 * F, D), dtype=w_gate.dtype, device=w_gate.device)
+        dn = torch.empty((E, D, F), dtype=w_gate.dtype, device=w_gate.device)
+    else:
+        gu, dn = out
+        if (gu.numel() != E * 2 * F * D or dn.numel() != E * D * F or not gu.is_contiguous()
+                or not dn.is_contiguous() or gu.dtype != w_gate.dtype or dn.dtype != w_gate.dtype):
+            raise ValueError("out tensors do not match the weights")
     _check(lib().llep_pack_weights(E, D, F, code, _ptr(w_gate), _ptr(w_up), _ptr(w_down),
                                    _ptr(gu), _ptr(dn), _stream(stream)), "llep_pack_weights")
     return gu, dn
