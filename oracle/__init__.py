@@ -10,6 +10,13 @@ plain counting for the permutation, float64 numpy arithmetic for the expert
 outputs. Each function cites the passage of the paper it follows.
 """
 
+from .backward import (  # noqa: F401
+    combine_backward,
+    moe_backward,
+    plan_backward,
+    silu_grad,
+    swiglu_ffn_backward,
+)
 from .llep import (  # noqa: F401
     PlanResult,
     bypass_to_standard_ep,
