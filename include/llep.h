@@ -205,11 +205,79 @@ int llep_grouped_ffn(const llep_plan_params *params,
 /* Step 5. y[t] = sum over k = 0..K-1 (ascending) of
  *   topk_gates[t*K+k] * out_perm[pair_row[t*K+k]]
  * in float32, rounded once to dtype; pairs with pair_row < 0 are skipped.
+ * topk_gates may be null: every gate is then 1 (this sums the per-pair
+ * input gradients dx_perm of llep_grouped_ffn_backward into dx).
  * out_perm [T*K][D], y [T][D] in `dtype`.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
 int llep_combine(const llep_plan_params *params, const void *out_perm,
                  const int32_t *pair_row, const float *topk_gates, int32_t D,
                  llep_dtype dtype, void *y, hipStream_t stream);
+
+/* ---- backward (bf16) ------------------------------------------------------
+ * The paper keeps LLEP exact under training: the gradients of the spilled
+ * chunks computed on foreign devices go back to the expert's native device
+ * and are added there (Sec. 1; Sec. 4). These calls give the backward of the
+ * five steps above; the plan and permutation of the forward are reused.
+ */
+
+/* Backward of Eq. (1). For every pair p = t*K + k with r = pair_row[p] >= 0:
+ *   d_out_perm[r] = topk_gates[p] * dy[t]        (rounded once to bf16)
+ *   d_gates[p]    = sum_i dy[t][i] * out_perm[r][i]   (float32)
+ * and d_gates[p] = 0 when pair_row[p] < 0. out_perm [T*K][D] (the forward's
+ * expert outputs), dy [T][D], d_out_perm [T*K][D], d_gates [T*K] float32.
+ * Requires dtype == LLEP_BF16.
+ * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
+int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
+                          const int32_t *pair_row, const float *topk_gates,
+                          const void *dy, int32_t D, llep_dtype dtype,
+                          void *d_out_perm, float *d_gates, hipStream_t stream);
+
+/* Packed weights of the backward GEMMs (untimed setup), same sizes as
+ * llep_packed_gate_up_bytes / llep_packed_down_bytes, same block layout as
+ * llep_pack_weights:
+ *   w_gate_up_t_packed [E][D*2F]: K = 2F; P row d, k = 64j + c holds
+ *                                 w_gate[d][32j + c], k = 64j + 32 + c holds
+ *                                 w_up[d][32j + c] (the forward's gate/up
+ *                                 interleave along the contraction);
+ *   w_down_t_packed    [E][F*D]:  K = D; P row f = row f of w_down.
+ * Requires dtype == LLEP_BF16, D % 64 == 0, F % 64 == 0.
+ * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
+int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype,
+                               const void *w_gate, const void *w_up,
+                               const void *w_down, void *w_gate_up_t_packed,
+                               void *w_down_t_packed, hipStream_t stream);
+
+/* Backward of step 4 for the groups of `device` (or of all devices when
+ * device == -1). With X = x_perm[rows of a group (d, e, s, n)] and
+ * dO = d_out_perm[same rows] (from llep_combine_backward):
+ *   g = X Wg_e, u = X Wu_e (recomputed, rounded to bf16), dA = dO Wd_e^T,
+ *   dg = dA * u * silu'(g), du = dA * silu(g), act = silu(g) * u
+ *   dx_perm[rows] = dg Wg_e^T + du Wu_e^T               (bf16)
+ * and, per expert e with groups in the range, the weight gradients in
+ * float32 (dw_gate, dw_up [E][D][F], dw_down [E][F][D]):
+ *   dWg_e = sum over e's groups of X^T dg, dWu_e of X^T du, dWd_e of act^T dO
+ * summed in gradient-return order: the group on e's native device (e / M)
+ * first, then the groups on other devices by increasing device index. For
+ * device == d these are d's partial gradients; for device == -1 they are the
+ * totals each native device holds after the gradient return. Experts without
+ * a group in the range are not written; rows outside the range are not
+ * written. Weights are the llep_pack_weights (w_gate_up_packed) and
+ * llep_pack_weights_backward outputs. Workspace of at least
+ * llep_grouped_ffn_backward_workspace_bytes bytes, 256-byte aligned.
+ * Requires dtype == LLEP_BF16, D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned.
+ * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */
+size_t llep_grouped_ffn_backward_workspace_bytes(const llep_plan_params *params,
+                                                 int32_t D, int32_t F,
+                                                 llep_dtype dtype);
+int llep_grouped_ffn_backward(const llep_plan_params *params,
+                              const llep_plan_buffers *plan, int32_t device,
+                              const void *x_perm, const void *d_out_perm,
+                              const void *w_gate_up_packed,
+                              const void *w_gate_up_t_packed,
+                              const void *w_down_t_packed, int32_t D, int32_t F,
+                              llep_dtype dtype, void *dx_perm, float *dw_gate,
+                              float *dw_up, float *dw_down, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
 
 /* Text of the calling thread's last error ("" if none). */
 const char *llep_last_error(void);

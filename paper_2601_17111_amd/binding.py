@@ -32,7 +32,9 @@ EXPORTED = [
     "llep_plan", "llep_permute", "llep_grouped_ffn", "llep_combine",
     "llep_pack_weights", "llep_plan_max_chunks", "llep_plan_rank_base_elems",
     "llep_grouped_ffn_workspace_bytes", "llep_packed_gate_up_bytes",
-    "llep_packed_down_bytes", "llep_last_error",
+    "llep_packed_down_bytes", "llep_last_error", "llep_combine_backward",
+    "llep_pack_weights_backward", "llep_grouped_ffn_backward_workspace_bytes",
+    "llep_grouped_ffn_backward",
 ]
 
 
@@ -92,6 +94,14 @@ def lib() -> ctypes.CDLL:
             "llep_grouped_ffn": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, i32, i32,
                                                 ctypes.c_int, _P, _P, sz, _P]),
             "llep_combine": (ctypes.c_int, [pp, _P, _P, _P, i32, ctypes.c_int, _P, _P]),
+            "llep_combine_backward": (ctypes.c_int, [pp, _P, _P, _P, _P, i32, ctypes.c_int, _P,
+                                                     _P, _P]),
+            "llep_pack_weights_backward": (ctypes.c_int, [i32, i32, i32, ctypes.c_int, _P, _P,
+                                                          _P, _P, _P, _P]),
+            "llep_grouped_ffn_backward_workspace_bytes": (sz, [pp, i32, i32, ctypes.c_int]),
+            "llep_grouped_ffn_backward": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, _P, _P, i32,
+                                                         i32, ctypes.c_int, _P, _P, _P, _P, _P,
+                                                         sz, _P]),
             "llep_last_error": (ctypes.c_char_p, []),
         }
         for name, (res, args) in sigs.items():
@@ -155,6 +165,12 @@ def llep_plan_rank_base_elems(params: llep_plan_params) -> int:
 
 def llep_grouped_ffn_workspace_bytes(params: llep_plan_params, F: int, dtype_code: int) -> int:
     return lib().llep_grouped_ffn_workspace_bytes(ctypes.byref(params), F, dtype_code)
+
+
+def llep_grouped_ffn_backward_workspace_bytes(params: llep_plan_params, D: int, F: int,
+                                              dtype_code: int) -> int:
+    return lib().llep_grouped_ffn_backward_workspace_bytes(ctypes.byref(params), D, F,
+                                                           dtype_code)
 
 
 # ---- plan buffers (device tensors) --------------------------------------------
@@ -237,3 +253,39 @@ def llep_combine(params: llep_plan_params, out_perm, pair_row, topk_gates, y, st
     _check(lib().llep_combine(ctypes.byref(params), _ptr(out_perm), _ptr(pair_row),
                               _ptr(topk_gates), out_perm.shape[-1], _dtype_code(out_perm),
                               _ptr(y), _stream(stream)), "llep_combine")
+
+
+# ---- backward ------------------------------------------------------------------
+
+def llep_combine_backward(params: llep_plan_params, out_perm, pair_row, topk_gates, dy,
+                          d_out_perm, d_gates, stream=None):
+    _check(lib().llep_combine_backward(ctypes.byref(params), _ptr(out_perm), _ptr(pair_row),
+                                       _ptr(topk_gates), _ptr(dy), dy.shape[-1],
+                                       _dtype_code(dy), _ptr(d_out_perm), _ptr(d_gates),
+                                       _stream(stream)), "llep_combine_backward")
+
+
+def llep_pack_weights_backward(w_gate, w_up, w_down, stream=None):
+    """Packed weights of the backward GEMMs (see llep.h); returns
+    (gate_up_t, down_t)."""
+    import torch
+    E, D, F = w_gate.shape
+    gut = torch.empty((E, D, 2 * F), dtype=w_gate.dtype, device=w_gate.device)
+    dnt = torch.empty((E, F, D), dtype=w_gate.dtype, device=w_gate.device)
+    _check(lib().llep_pack_weights_backward(E, D, F, _dtype_code(w_gate), _ptr(w_gate),
+                                            _ptr(w_up), _ptr(w_down), _ptr(gut), _ptr(dnt),
+                                            _stream(stream)), "llep_pack_weights_backward")
+    return gut, dnt
+
+
+def llep_grouped_ffn_backward(params: llep_plan_params, bufs: PlanBuffers, device: int, x_perm,
+                              d_out_perm, w_gate_up, w_gate_up_t, w_down_t, dx_perm, dw_gate,
+                              dw_up, dw_down, workspace, stream=None):
+    D = x_perm.shape[-1]
+    F = w_down_t.shape[-2]
+    _check(lib().llep_grouped_ffn_backward(
+        ctypes.byref(params), ctypes.byref(bufs.struct), device, _ptr(x_perm), _ptr(d_out_perm),
+        _ptr(w_gate_up), _ptr(w_gate_up_t), _ptr(w_down_t), D, F, _dtype_code(x_perm),
+        _ptr(dx_perm), _ptr(dw_gate), _ptr(dw_up), _ptr(dw_down), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)),
+        "llep_grouped_ffn_backward")

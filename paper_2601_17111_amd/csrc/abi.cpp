@@ -217,7 +217,8 @@ int llep_combine(const llep_plan_params *params, const void *out_perm, const int
   int rc = check_params(params);
   if (rc != LLEP_OK) return rc;
   if ((rc = check_rows(D, dtype)) != LLEP_OK) return rc;
-  if (params->T > 0 && (!out_perm || !pair_row || !topk_gates || !y))
+  // topk_gates == nullptr: every gate is 1 (sums the pairs' input gradients)
+  if (params->T > 0 && (!out_perm || !pair_row || !y))
     return fail(LLEP_E_ARG, "a data pointer is null");
   if (!aligned16(out_perm) || !aligned16(y)) return fail(LLEP_E_ARG, "out_perm / y not 16-byte aligned");
   llep::CombineArgs a;
@@ -230,6 +231,103 @@ int llep_combine(const llep_plan_params *params, const void *out_perm, const int
   a.gates = topk_gates;
   a.y = y;
   return hip_result(llep::launch_combine(a, stream), "llep_combine");
+}
+
+int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
+                          const int32_t *pair_row, const float *topk_gates, const void *dy,
+                          int32_t D, llep_dtype dtype, void *d_out_perm, float *d_gates,
+                          hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if ((rc = check_rows(D, dtype)) != LLEP_OK) return rc;
+  if (dtype != LLEP_BF16) return fail(LLEP_E_DTYPE, "the backward supports bf16 only");
+  if (params->T > 0 && (!out_perm || !pair_row || !topk_gates || !dy || !d_out_perm || !d_gates))
+    return fail(LLEP_E_ARG, "a data pointer is null");
+  if (!aligned16(out_perm) || !aligned16(dy) || !aligned16(d_out_perm))
+    return fail(LLEP_E_ARG, "out_perm / dy / d_out_perm not 16-byte aligned");
+  llep::CombineBwdArgs a;
+  a.T = params->T;
+  a.K = params->K;
+  a.D = D;
+  a.out_perm = out_perm;
+  a.dy = dy;
+  a.pair_row = pair_row;
+  a.gates = topk_gates;
+  a.d_out_perm = d_out_perm;
+  a.d_gates = d_gates;
+  return hip_result(llep::launch_combine_backward(a, stream), "llep_combine_backward");
+}
+
+int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype,
+                               const void *w_gate, const void *w_up, const void *w_down,
+                               void *w_gate_up_t_packed, void *w_down_t_packed,
+                               hipStream_t stream) {
+  if (E < 1 || E > LLEP_MAX_EXPERTS) return fail(LLEP_E_ARG, "E outside [1, LLEP_MAX_EXPERTS]");
+  int rc = check_ffn_dims(D, F, dtype);
+  if (rc != LLEP_OK) return rc;
+  if (dtype != LLEP_BF16) return fail(LLEP_E_DTYPE, "the backward supports bf16 only");
+  if (!w_gate || !w_up || !w_down || !w_gate_up_t_packed || !w_down_t_packed)
+    return fail(LLEP_E_ARG, "a weight pointer is null");
+  if (!aligned16(w_gate_up_t_packed) || !aligned16(w_down_t_packed))
+    return fail(LLEP_E_ARG, "packed weights not 16-byte aligned");
+  return hip_result(llep::launch_pack_backward(E, D, F, w_gate, w_up, w_down, w_gate_up_t_packed,
+                                               w_down_t_packed, stream),
+                    "llep_pack_weights_backward");
+}
+
+size_t llep_grouped_ffn_backward_workspace_bytes(const llep_plan_params *params, int32_t D,
+                                                 int32_t F, llep_dtype dtype) {
+  if (check_params(params) != LLEP_OK || D < 1 || F < 1 || dtype != LLEP_BF16) return 0;
+  return llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F);
+}
+
+int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_buffers *plan,
+                              int32_t device, const void *x_perm, const void *d_out_perm,
+                              const void *w_gate_up_packed, const void *w_gate_up_t_packed,
+                              const void *w_down_t_packed, int32_t D, int32_t F,
+                              llep_dtype dtype, void *dx_perm, float *dw_gate, float *dw_up,
+                              float *dw_down, void *workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if ((rc = check_plan_buffers(plan)) != LLEP_OK) return rc;
+  if ((rc = check_ffn_dims(D, F, dtype)) != LLEP_OK) return rc;
+  if (dtype != LLEP_BF16) return fail(LLEP_E_DTYPE, "the backward supports bf16 only");
+  if (device < -1 || device >= params->P) return fail(LLEP_E_ARG, "device outside [-1, P)");
+  if (!x_perm || !d_out_perm || !w_gate_up_packed || !w_gate_up_t_packed || !w_down_t_packed ||
+      !dx_perm || !dw_gate || !dw_up || !dw_down)
+    return fail(LLEP_E_ARG, "a data pointer is null");
+  if (!aligned16(x_perm) || !aligned16(d_out_perm) || !aligned16(w_gate_up_packed) ||
+      !aligned16(w_gate_up_t_packed) || !aligned16(w_down_t_packed) || !aligned16(dx_perm) ||
+      !aligned16(dw_gate) || !aligned16(dw_up) || !aligned16(dw_down))
+    return fail(LLEP_E_ARG, "data not 16-byte aligned");
+  const size_t need =
+      llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F);
+  if (!workspace || workspace_bytes < need)
+    return fail(LLEP_E_WORKSPACE,
+                "workspace missing or smaller than llep_grouped_ffn_backward_workspace_bytes");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(LLEP_E_WORKSPACE, "workspace not 256-byte aligned");
+  llep::FfnBwdArgs a;
+  a.R = params->T * params->K;
+  a.P = params->P;
+  a.E = params->E;
+  a.D = D;
+  a.F = F;
+  a.device = device;
+  a.groups = plan->groups;
+  a.group_begin = plan->group_begin;
+  a.x_perm = x_perm;
+  a.d_out_perm = d_out_perm;
+  a.w_gate_up = w_gate_up_packed;
+  a.w_gate_up_t = w_gate_up_t_packed;
+  a.w_down_t = w_down_t_packed;
+  a.dx_perm = dx_perm;
+  a.dw_gate = dw_gate;
+  a.dw_up = dw_up;
+  a.dw_down = dw_down;
+  a.ws = workspace;
+  return hip_result(llep::launch_grouped_ffn_backward(a, stream), "llep_grouped_ffn_backward");
 }
 
 }  // extern "C"

@@ -117,17 +117,35 @@ __global__ __launch_bounds__(256) void tile_table_kernel(const int32_t *__restri
 // bf16 MFMA grouped GEMM: C[m][n] = sum_k A[m][k] B_e[n][k]
 // ---------------------------------------------------------------------------
 
+// Epilogues: the forward projections (plain bf16 C, or SwiGLU of gate/up
+// column pairs), the SwiGLU backward (C = d act; reads the recomputed gate /
+// up values, writes their gradients and the activation), and the two weight
+// gradients (fp32, per expert; gate/up columns de-interleaved).
+enum Epilogue : int { kEpiPlain = 0, kEpiSwiglu = 1, kEpiSwigluBwd = 2, kEpiWgradGU = 3,
+                      kEpiWgradD = 4 };
+
 struct GemmArgs {
   const uint16_t *A;
-  int64_t lda;
+  int64_t lda;           // row-major A: elements per row
+  int64_t a_blk_stride;  // blocked A: bytes per 16-row block across all of K
   const uint16_t *B;
-  int64_t b_expert_stride;
+  int64_t b_expert_stride;  // elements between experts' packed B
+  int64_t b_blk_stride;     // bytes per 16-row block of B across all of K
   uint16_t *C;
   int64_t ldc;
   const int32_t *groups;
-  const int4 *tiles;
+  const int4 *tiles;        // forward: (group, m-tile, padded first row, 0)
   const int32_t *n_mtiles;
   int32_t N, Kdim;
+  // SwiGLU backward
+  const uint16_t *GU;  // blocked [padded rows][2F]: gate / up values
+  uint16_t *act;       // blocked [padded rows][F]
+  // weight gradients: C is M x N per expert (fp32), over a k-segment per expert
+  int32_t M;
+  const int4 *wg_experts;  // (expert, first k-slice, k-slices, 0)
+  const int32_t *n_wg;
+  float *Cf, *Cf2;         // dW (gate part / down) and the up part
+  int64_t cf_expert_stride;
 };
 
 
@@ -215,7 +233,7 @@ __device__ __forceinline__ int lds_swz32(int row, int kc) {
 }
 
 struct TileCoord {
-  int e, row0, prow0, m0, rows_valid, n0, cols_valid;
+  int e, row0, prow0, m0, rows_valid, n0, cols_valid, k0, nk;
 };
 
 template <int BM, int BN>
@@ -235,12 +253,34 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, 
   t.rows_valid = min(BM, gr[3] - t.m0);
   t.n0 = nt * BN;
   t.cols_valid = min(BN, g.N - t.n0);
+  t.k0 = 0;
+  t.nk = g.Kdim / kSK;
+  return true;
+}
+
+// weight-gradient tiles: (expert, m-tile, n-tile) over M x N, expert-major;
+// the contraction runs over the expert's k-segment
+template <int BM, int BN>
+__device__ __forceinline__ bool decode_tile_wg(const GemmArgs &g, int u, int n_exp, TileCoord &t) {
+  const int n_mt = (g.M + BM - 1) / BM, n_nt = (g.N + BN - 1) / BN;
+  if (u >= n_exp * n_mt * n_nt) return false;
+  const int i = u / (n_mt * n_nt), rem = u - i * (n_mt * n_nt);
+  const int4 we = g.wg_experts[i];
+  t.e = we.x;
+  t.row0 = 0;
+  t.prow0 = 0;
+  t.m0 = (rem / n_nt) * BM;
+  t.rows_valid = min(BM, g.M - t.m0);
+  t.n0 = (rem % n_nt) * BN;
+  t.cols_valid = min(BN, g.N - t.n0);
+  t.k0 = we.y;
+  t.nk = we.z;
   return true;
 }
 
 // A is row-major (lda) or, with kABlocked, in 16 x 32 blocks over padded
 // rows; C likewise with kCBlocked. B is always in 16 x 32 blocks.
-template <int BN, int WAVES_M, int WAVES_N, bool kSwiglu, bool kABlocked, bool kCBlocked>
+template <int BN, int WAVES_M, int WAVES_N, int kEpi, bool kABlocked, bool kCBlocked>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
 __attribute__((amdgpu_waves_per_eu(WAVES_M * WAVES_N / 4, WAVES_M * WAVES_N / 4)))
 void gemm256_kernel(GemmArgs g) {
@@ -248,6 +288,8 @@ void gemm256_kernel(GemmArgs g) {
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr bool kSwiglu = kEpi == kEpiSwiglu;
+  constexpr bool kWgrad = kEpi == kEpiWgradGU || kEpi == kEpiWgradD;
   // DMA blocks (16 rows each) per stage, dealt round-robin over the waves:
   // every wave has A_PER_WAVE A blocks and B_FULL B blocks, the first B_REM
   // waves one B block more. Waits count the PER_STAGE instructions every
@@ -278,32 +320,37 @@ void gemm256_kernel(GemmArgs g) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const int n_mt = *g.n_mtiles;
+  const int n_mt = kWgrad ? 0 : *g.n_mtiles;
+  const int n_exp = kWgrad ? *g.n_wg : 0;
   const int n_nt = (g.N + BN - 1) / BN;
   const int G = gridDim.x;  // a multiple of 8
   const int slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
-  const int nk = g.Kdim / kSK;
+  auto decode = [&](int u, TileCoord &c) {
+    return kWgrad ? decode_tile_wg<BM, BN>(g, u, n_exp, c) : decode_tile<BM, BN>(g, u, n_mt, n_nt, c);
+  };
   const int kc_load = (lane & 3) ^ ((lane >> 4) & 3);
   const int64_t lda_b = g.lda * 2;
   // a 16 x 32 block is 1 KB; lane l fills LDS bytes 16l .. 16l+15 = row
   // l / 4, chunk slot l % 4, which holds logical chunk kc_load of that row
   const int32_t blk_lane = (lane >> 2) * 64 + kc_load * 16;
-  const int64_t blk_row_b = int64_t(nk) * 1024;  // one 16-row block across K
   const uint32_t sA0 = lds_addr(smem), sB0 = sA0 + A_STAGE_BYTES;
 
   TileCoord t;
-  if (!decode_tile<BM, BN>(g, slot, n_mt, n_nt, t)) return;
+  if (!decode(slot, t)) return;
   const char *Ab, *Bb;
   int32_t offA[A_PER_WAVE], offB[B_SLOTS];
   auto setup = [&](const TileCoord &c) {
     // rows (columns) past the tile's valid ones re-read its last valid row
     // (block), so every address stays in bounds
     if (kABlocked) {
-      Ab = reinterpret_cast<const char *>(g.A) + ((c.prow0 + c.m0) >> 4) * blk_row_b;
+      // forward: padded rows of the group; weight gradients: rows of the
+      // expert's M x K operand, from its k-segment on
+      const int64_t rb0 = kWgrad ? (c.m0 >> 4) : ((c.prow0 + c.m0) >> 4);
+      Ab = reinterpret_cast<const char *>(g.A) + rb0 * g.a_blk_stride + int64_t(c.k0) * 1024;
 #pragma unroll
       for (int j = 0; j < A_PER_WAVE; ++j) {
         const int rb = min(wave + NWD * j, (c.rows_valid - 1) >> 4);
-        offA[j] = int32_t(rb * blk_row_b + blk_lane);
+        offA[j] = int32_t(rb * g.a_blk_stride + blk_lane);
       }
     } else {
       Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
@@ -314,11 +361,11 @@ void gemm256_kernel(GemmArgs g) {
       }
     }
     Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
-         (c.n0 >> 4) * blk_row_b;
+         (c.n0 >> 4) * g.b_blk_stride + int64_t(c.k0) * 1024;
 #pragma unroll
     for (int j = 0; j < B_SLOTS; ++j) {
       const int nb = min(wave + NWD * j, (c.cols_valid - 1) >> 4);
-      offB[j] = int32_t(nb * blk_row_b + blk_lane);
+      offB[j] = int32_t(nb * g.b_blk_stride + blk_lane);
     }
   };
   // request slice kt into stage st: 64 B per row along K for a row-major A,
@@ -339,7 +386,7 @@ void gemm256_kernel(GemmArgs g) {
   auto prologue = [&]() {
 #pragma unroll
     for (int k = 0; k < kAhead; ++k)
-      if (k < nk) issue(k, k);
+      if (k < t.nk) issue(k, k);
   };
   setup(t);
   prologue();
@@ -421,6 +468,7 @@ void gemm256_kernel(GemmArgs g) {
   };
 
   for (int it = 0;; ++it) {
+    const int nk = t.nk;
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -474,7 +522,7 @@ void gemm256_kernel(GemmArgs g) {
     // every wave is done with the ring before the next tile's slices land
     __syncthreads();
     const TileCoord c = t;
-    const bool more = decode_tile<BM, BN>(g, (it + 1) * G + slot, n_mt, n_nt, t);
+    const bool more = decode((it + 1) * G + slot, t);
     // the next tile's first kAhead - 1 slices load during the epilogue; the
     // last stages hold the epilogue's staging area until the barrier below
     static_assert(kStages - (kAhead - 1) >= 2, "two stages free for staging");
@@ -482,7 +530,7 @@ void gemm256_kernel(GemmArgs g) {
       setup(t);
 #pragma unroll
       for (int k = 0; k < kAhead - 1; ++k)
-        if (k < nk) issue(k, k);
+        if (k < t.nk) issue(k, k);
     }
 
     // Epilogue. The MFMAs take the weight fragment as their first operand,
@@ -536,9 +584,114 @@ void gemm256_kernel(GemmArgs g) {
               *reinterpret_cast<const i32x4 *>(sp + rb * 1024 + lane * 16);
         }
       }
+    } else if constexpr (kEpi == kEpiPlain && kCBlocked) {
+      // blocked C over padded rows: per 32-column block, one 1 KB block per
+      // 16 rows of the wave's part
+      static_assert((WM / 16) * 1024 <= STAGING, "staging");
+      const int64_t rb0 = (c.prow0 + c.m0 + wm * WM) >> 4;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int col0 = c.n0 + wn * WN + j * 32;
+        if (col0 >= g.N) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          char *blk = stg + (2 * i + ((lane & 31) >> 4)) * 1024 + (lane & 15) * 64;
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq)
+            *reinterpret_cast<uint2 *>(blk + (8 * gq + 4 * h) * 2) =
+                make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
+                           pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
+        }
+        char *dst = reinterpret_cast<char *>(g.C) + (rb0 * (g.ldc >> 5) + (col0 >> 5)) * 1024 +
+                    lane * 16;
+#pragma unroll
+        for (int rb = 0; rb < WM / 16; ++rb) {
+          if (rb * 16 >= rows_w) break;
+          *reinterpret_cast<i32x4 *>(dst + int64_t(rb) * (g.ldc >> 5) * 1024) =
+              *reinterpret_cast<const i32x4 *>(stg + rb * 1024 + lane * 16);
+        }
+      }
+    } else if constexpr (kEpi == kEpiSwigluBwd) {
+      // C = d act [padded rows][F] for activation columns f. With g = gate,
+      // u = up (recomputed, blocked [padded rows][2F], gate f at column
+      // 64 (f / 32) + f % 32, up 32 further): d gate = d act u silu'(g),
+      // d up = d act silu(g), written in the same layout, and act = silu(g) u
+      // (blocked [padded rows][F]) for the down projection's weight gradient.
+      static_assert(kCBlocked, "gate/up gradients are blocked over padded rows");
+      const int F = int(g.ldc);
+      const int gu_blocks = (2 * F) >> 5, a_blocks = F >> 5;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        if (i * 32 >= rows_w) break;
+        const int pr = c.prow0 + c.m0 + wm * WM + i * 32 + (lane & 31);
+        const bool row_ok = i * 32 + (lane & 31) < rows_w;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col0 = c.n0 + wn * WN + j * 32;  // first activation column f
+          if (col0 >= g.N || !row_ok) continue;
+          const int64_t gblk = (int64_t(pr >> 4) * gu_blocks + (col0 >> 5) * 2) * 512 +
+                               (pr & 15) * 32;
+          const int64_t ablk = (int64_t(pr >> 4) * a_blocks + (col0 >> 5)) * 512 + (pr & 15) * 32;
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+            const int cc = 8 * gq + 4 * h;  // column inside the 32-block
+            const uint2 gw = *reinterpret_cast<const uint2 *>(g.GU + gblk + cc);
+            const uint2 uw = *reinterpret_cast<const uint2 *>(g.GU + gblk + 512 + cc);
+            float dg[4], du[4], av[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const uint32_t gbits = (e < 2 ? gw.x : gw.y) >> (16 * (e & 1));
+              const uint32_t ubits = (e < 2 ? uw.x : uw.y) >> (16 * (e & 1));
+              const float gv = __uint_as_float(gbits << 16), uv = __uint_as_float(ubits << 16);
+              const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-gv));
+              const float da = acc[i][j][4 * gq + e];
+              dg[e] = da * uv * (sg * (1.0f + gv * (1.0f - sg)));
+              du[e] = da * (gv * sg);
+              av[e] = gv * sg * uv;
+            }
+            uint16_t *dgu = g.C;
+            *reinterpret_cast<uint2 *>(dgu + gblk + cc) =
+                make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
+            *reinterpret_cast<uint2 *>(dgu + gblk + 512 + cc) =
+                make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));
+            *reinterpret_cast<uint2 *>(g.act + ablk + cc) =
+                make_uint2(pack2(av[0], av[1]), pack2(av[2], av[3]));
+          }
+        }
+      }
+    } else if constexpr (kWgrad) {
+      // fp32 weight gradient of expert c.e: C[m][n], rows m < M, written as
+      // 16-byte runs of 4 columns. Gate/up mode: column n = 64 q + cc is
+      // gate column 32 q + cc (cc < 32) or up column 32 q + cc - 32.
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int m = c.m0 + wm * WM + i * 32 + (lane & 31);
+        if (i * 32 >= rows_w) break;
+        if (i * 32 + (lane & 31) >= rows_w) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col0 = c.n0 + wn * WN + j * 32;
+          if (col0 >= g.N) continue;
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+            const int n = col0 + 8 * gq + 4 * h;
+            float *dst;
+            if (kEpi == kEpiWgradGU) {
+              const int q = n >> 6, cc = n & 63;
+              const int Fo = g.N >> 1;
+              dst = (cc < 32 ? g.Cf : g.Cf2) + int64_t(c.e) * g.cf_expert_stride + int64_t(m) * Fo +
+                    32 * q + (cc & 31);
+            } else {
+              dst = g.Cf + int64_t(c.e) * g.cf_expert_stride + int64_t(m) * g.N + n;
+            }
+            *reinterpret_cast<f32x4 *>(dst) = f32x4{acc[i][j][4 * gq], acc[i][j][4 * gq + 1],
+                                                    acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]};
+          }
+        }
+      }
     } else {
       // row-major C: 32 rows x WN columns per piece, rows RS bytes apart
-      static_assert(!kCBlocked, "blocked C is written by the SwiGLU epilogue only");
+      static_assert(!kCBlocked, "blocked C: other epilogues");
       constexpr int RS = WN * 2;
       constexpr int CH = WN / 8;  // 16-byte chunks per row segment
       static_assert(32 * RS <= STAGING, "staging");
@@ -570,7 +723,7 @@ void gemm256_kernel(GemmArgs g) {
       // staging reads are done (lgkmcnt) before slice kAhead - 1 may land
       // there; the DMAs and stores in flight are not waited for
       wait_and_sync<63>();
-      if (kAhead - 1 < nk) issue(kAhead - 1, kAhead - 1);
+      if (kAhead - 1 < t.nk) issue(kAhead - 1, kAhead - 1);
     }
     if (!more) break;
   }
@@ -678,11 +831,12 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
                        a.device, a.P, kTileM, tiles, n_mtiles);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    GemmArgs g1;
+    GemmArgs g1 = {};
     g1.A = static_cast<const uint16_t *>(a.x_perm);
     g1.lda = a.D;
     g1.B = static_cast<const uint16_t *>(a.w_gate_up);
     g1.b_expert_stride = int64_t(2) * a.F * a.D;
+    g1.b_blk_stride = int64_t(a.D / kSK) * 1024;
     g1.C = static_cast<uint16_t *>(act);
     g1.ldc = a.F;
     g1.groups = a.groups;
@@ -691,26 +845,28 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g1.N = 2 * a.F;
     g1.Kdim = a.D;
     constexpr int NT = 64 * kWavesM * kWavesN;
-    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, true, false, true>), dim3(grid),
-                       dim3(NT), 0, stream, g1);
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiSwiglu, false, true>),
+                       dim3(grid), dim3(NT), 0, stream, g1);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g2 = g1;
     g2.A = static_cast<const uint16_t *>(act);
     g2.lda = a.F;
+    g2.a_blk_stride = int64_t(a.F / kSK) * 1024;
     g2.B = static_cast<const uint16_t *>(a.w_down);
     g2.b_expert_stride = int64_t(a.D) * a.F;
+    g2.b_blk_stride = int64_t(a.F / kSK) * 1024;
     g2.C = static_cast<uint16_t *>(a.out_perm);
     g2.ldc = a.D;
     g2.N = a.D;
     g2.Kdim = a.F;
     // the down projection's N is D: 192-wide tiles divide D = 2880 exactly
     if (a.D % 256 != 0 && a.D % 192 == 0)
-      hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, false, true, false>),
+      hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiPlain, true, false>),
                          dim3(grid), dim3(64 * kWavesM192 * kWavesN192), 0, stream, g2);
     else
-      hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, false, true, false>), dim3(grid),
-                         dim3(NT), 0, stream, g2);
+      hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, true, false>),
+                         dim3(grid), dim3(NT), 0, stream, g2);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(ffn_f32_gate_up_kernel, dim3(1024), dim3(256), 0, stream,
@@ -774,6 +930,345 @@ hipError_t launch_pack(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const 
                        hipStream_t stream) {
   if (dtype == LLEP_BF16) return pack_typed<uint16_t>(E, D, F, w_gate, w_up, w_down, gu, dn, stream);
   return pack_typed<float>(E, D, F, w_gate, w_up, w_down, gu, dn, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Backward of the grouped SwiGLU FFN (bf16), for the groups of one device or
+// of all devices. Given d out for the groups' rows (from the combine's
+// backward):
+//   1. recompute g, u = X [Wg | Wu]             (blocked over padded rows)
+//   2. d act = d out Wd^T; epilogue: d g, d u and act = silu(g) u
+//   3. dX = [d g | d u] [Wg | Wu]^T               (x_perm rows)
+//   4. weight gradients, in fp32 per expert: the rows of an expert's groups
+//      are laid end to end in gradient-return order (the group on the
+//      expert's native device first, then the other devices in increasing
+//      order; each group padded with zero rows to a multiple of 32), and
+//      dWg | dWu = X^T [d g | d u], dWd = act^T d out contract over that
+//      segment, so an expert's gradient sums its native partial and then the
+//      returned partials, in a fixed order.
+// ---------------------------------------------------------------------------
+
+struct BwdLayout {
+  size_t tiles_off, wge_off, kbase_off, gprow_off, chunk_off;
+  size_t gu_off, dgu_off, act_off, xt_off, dot_off, actt_off, dgut_off, total;
+  int64_t max_groups, max_mtiles, prow_max, kmax;
+};
+
+static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
+
+static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F) {
+  BwdLayout L;
+  L.max_groups = 2 * int64_t(E) + P;
+  L.max_mtiles = R / kTileM + L.max_groups + 1;
+  L.prow_max = R + 16 * L.max_groups;
+  L.kmax = (R + 32 * L.max_groups + 31) / 32 * 32;
+  size_t o = 256;  // counters: n_mtiles, n_wg, k-slices in use
+  L.tiles_off = o;  o = round256(o + size_t(L.max_mtiles) * 16);
+  L.wge_off = o;    o = round256(o + size_t(E) * 16);
+  L.kbase_off = o;  o = round256(o + size_t(L.max_groups) * 4);
+  L.gprow_off = o;  o = round256(o + size_t(L.max_groups) * 4);
+  L.chunk_off = o;  o = round256(o + size_t(L.kmax / 32) * 4);
+  L.gu_off = o;     o = round256(o + size_t(L.prow_max) * 2 * F * 2);
+  L.dgu_off = o;    o = round256(o + size_t(L.prow_max) * 2 * F * 2);
+  L.act_off = o;    o = round256(o + size_t(L.prow_max) * F * 2);
+  L.xt_off = o;     o = round256(o + size_t(D) * L.kmax * 2);
+  L.dot_off = o;    o = round256(o + size_t(D) * L.kmax * 2);
+  L.actt_off = o;   o = round256(o + size_t(F) * L.kmax * 2);
+  L.dgut_off = o;   o = round256(o + size_t(2 * F) * L.kmax * 2);
+  L.total = o;
+  return L;
+}
+
+size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F) {
+  return bwd_layout(R, E, P, D, F).total;
+}
+
+// One workgroup. For the groups [lo, hi) of the range: each group's first
+// weight-gradient row (kbase, a multiple of 32) in gradient-return order, its
+// first padded forward row (gprow, rows rounded to 16 per group, as the
+// tile list lays them out), the owner group of every 32-row chunk, and the
+// experts present with their segment (first 32-row slice, slices).
+__global__ __launch_bounds__(1024) void wgrad_table_kernel(
+    const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
+    int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase, int32_t *__restrict__ gprow,
+    int32_t *__restrict__ chunk_group, int4 *__restrict__ wg_experts, int32_t *__restrict__ n_wg,
+    int32_t *__restrict__ kslices) {
+  __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks], s16[kMaxChunks];
+  __shared__ int32_t present[LLEP_MAX_EXPERTS];
+  const int tid = threadIdx.x;
+  const int lo = device < 0 ? group_begin[0] : group_begin[device];
+  const int hi = device < 0 ? group_begin[P] : group_begin[device + 1];
+  const int G = min(hi - lo, kMaxChunks);
+  for (int i = tid; i < G; i += blockDim.x) {
+    const int32_t *gr = groups + 4 * (lo + i);
+    const int d = gr[0], e = gr[1], n = gr[3];
+    se[i] = e;
+    skey[i] = d == e / M ? -1 : d;  // native device first
+    ssl[i] = (n + 31) / 32;
+    s16[i] = (n + 15) / 16 * 16;
+  }
+  __syncthreads();
+  for (int i = tid; i < G; i += blockDim.x) {
+    int32_t kb = 0, pr = 0;
+    for (int j = 0; j < G; ++j) {
+      if (se[j] < se[i] || (se[j] == se[i] && skey[j] < skey[i])) kb += ssl[j];
+      if (j < i) pr += s16[j];
+    }
+    kbase[i] = kb * 32;
+    gprow[i] = pr;
+    for (int c = kb; c < kb + ssl[i]; ++c) chunk_group[c] = lo + i;
+  }
+  for (int e = tid; e < E; e += blockDim.x) {
+    int32_t sl = 0;
+    for (int j = 0; j < G; ++j) sl += se[j] == e ? ssl[j] : 0;
+    present[e] = sl > 0;
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += blockDim.x) {
+    if (!present[e]) continue;
+    int32_t idx = 0, start = 0, sl = 0;
+    for (int f = 0; f < e; ++f) idx += present[f];
+    for (int j = 0; j < G; ++j) {
+      start += se[j] < e ? ssl[j] : 0;
+      sl += se[j] == e ? ssl[j] : 0;
+    }
+    wg_experts[idx] = make_int4(e, start, sl, 0);
+  }
+  if (tid == 0) {
+    int32_t n = 0, tot = 0;
+    for (int e = 0; e < E; ++e) n += present[e];
+    for (int j = 0; j < G; ++j) tot += ssl[j];
+    *n_wg = n;
+    *kslices = tot;
+  }
+}
+
+// Copy C columns of the range's rows into the weight-gradient layout:
+// blocks of 16 columns x 32 rows over [C][kmax], row kbase[g] + r of the
+// layout = row r of group g (zero for the padding r >= n_g). The source is
+// row-major by x_perm row (ld elements) or blocked over padded rows.
+template <bool kBlocked>
+__global__ __launch_bounds__(256) void to_wgrad_kernel(
+    const uint16_t *__restrict__ src, int64_t ld, int32_t C, const int32_t *__restrict__ groups,
+    int32_t lo_dev, const int32_t *__restrict__ group_begin, int32_t P,
+    const int32_t *__restrict__ kbase, const int32_t *__restrict__ gprow,
+    const int32_t *__restrict__ chunk_group, const int32_t *__restrict__ kslices, int64_t kmax,
+    uint16_t *__restrict__ dst) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][40];
+  const int t = threadIdx.x;
+  const int lo = lo_dev < 0 ? group_begin[0] : group_begin[lo_dev];
+  const int64_t items = int64_t(*kslices) * (C / 64);
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int c = int(item / (C / 64)), cc = int(item % (C / 64));
+    const int gi = chunk_group[c], i = gi - lo;
+    const int n = groups[4 * gi + 3];
+    const int r0 = c * 32 - kbase[i];
+    {
+      const int r = t >> 3, col = cc * 64 + (t & 7) * 8;
+      i32x4 v = {0, 0, 0, 0};
+      const int row = r0 + r;
+      if (row < n) {
+        if (kBlocked) {
+          const int pr = gprow[i] + row;
+          v = *reinterpret_cast<const i32x4 *>(
+              src + (int64_t(pr >> 4) * (C >> 5) + (col >> 5)) * 512 + (pr & 15) * 32 + (col & 31));
+        } else {
+          v = *reinterpret_cast<const i32x4 *>(src + int64_t(groups[4 * gi + 2] + row) * ld + col);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        tile[(t & 7) * 8 + 2 * q][r] = uint16_t(uint32_t(v[q]) & 0xffffu);
+        tile[(t & 7) * 8 + 2 * q + 1][r] = uint16_t(uint32_t(v[q]) >> 16);
+      }
+    }
+    __syncthreads();
+    {
+      const int b = t >> 6, o = t & 63;
+      const int lc = b * 16 + (o >> 2), k8 = (o & 3) * 8;
+      *reinterpret_cast<i32x4 *>(dst + (int64_t(cc * 4 + b) * (kmax / 32) + c) * 512 + (o >> 2) * 32 +
+                                 k8) = *reinterpret_cast<const i32x4 *>(&tile[lc][k8]);
+    }
+    __syncthreads();
+  }
+}
+
+// Packed weights for the backward GEMMs, in the forward's block layout:
+// [Wg | Wu] rows d with the gate/up columns interleaved per 32 (K = 2F), and
+// Wd rows f (K = D).
+template <typename T>
+__global__ __launch_bounds__(256) void pack_bwd_kernel(const T *__restrict__ wg,
+                                                       const T *__restrict__ wu,
+                                                       const T *__restrict__ wd, T *__restrict__ gut,
+                                                       T *__restrict__ dnt, int32_t E, int32_t D,
+                                                       int32_t F) {
+  const int64_t per = int64_t(D) * F, total = int64_t(E) * per;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < total;
+       u += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t e = u / per, r = u % per;
+    // Wg, Wu [E][D][F]: element (d, f)
+    const int d = int(r / F), f = int(r % F);
+    const int j = 64 * (f / 32) + (f % 32);
+    gut[e * 2 * per + packed_index(d, j, 2 * F)] = wg[u];
+    gut[e * 2 * per + packed_index(d, j + 32, 2 * F)] = wu[u];
+    // Wd [E][F][D]: element (f2, d2) = row f2 of the (K = D) packing
+    const int f2 = int(r / D), d2 = int(r % D);
+    dnt[e * per + packed_index(f2, d2, D)] = wd[u];
+  }
+}
+
+hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, const void *w_gate,
+                                const void *w_up, const void *w_down, void *gut, void *dnt,
+                                hipStream_t stream) {
+  hipLaunchKernelGGL(pack_bwd_kernel<uint16_t>, dim3(4096), dim3(256), 0, stream,
+                     static_cast<const uint16_t *>(w_gate), static_cast<const uint16_t *>(w_up),
+                     static_cast<const uint16_t *>(w_down), static_cast<uint16_t *>(gut),
+                     static_cast<uint16_t *>(dnt), E, D, F);
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) {
+  const BwdLayout L = bwd_layout(a.R, a.E, a.P, a.D, a.F);
+  char *ws = static_cast<char *>(a.ws);
+  int32_t *n_mtiles = reinterpret_cast<int32_t *>(ws);
+  int32_t *n_wg = n_mtiles + 1;
+  int32_t *kslices = n_mtiles + 2;
+  int4 *tiles = reinterpret_cast<int4 *>(ws + L.tiles_off);
+  int4 *wge = reinterpret_cast<int4 *>(ws + L.wge_off);
+  int32_t *kbase = reinterpret_cast<int32_t *>(ws + L.kbase_off);
+  int32_t *gprow = reinterpret_cast<int32_t *>(ws + L.gprow_off);
+  int32_t *chunk = reinterpret_cast<int32_t *>(ws + L.chunk_off);
+  uint16_t *gu = reinterpret_cast<uint16_t *>(ws + L.gu_off);
+  uint16_t *dgu = reinterpret_cast<uint16_t *>(ws + L.dgu_off);
+  uint16_t *act = reinterpret_cast<uint16_t *>(ws + L.act_off);
+  uint16_t *xt = reinterpret_cast<uint16_t *>(ws + L.xt_off);
+  uint16_t *dot = reinterpret_cast<uint16_t *>(ws + L.dot_off);
+  uint16_t *actt = reinterpret_cast<uint16_t *>(ws + L.actt_off);
+  uint16_t *dgut = reinterpret_cast<uint16_t *>(ws + L.dgut_off);
+  const int grid = (cu_count() + 7) / 8 * 8;
+  const int D = a.D, F = a.F;
+  hipError_t err;
+#define LLEP_CHECK_LAUNCH()            \
+  do {                                 \
+    err = hipGetLastError();           \
+    if (err != hipSuccess) return err; \
+  } while (0)
+  hipLaunchKernelGGL(tile_table_kernel, dim3(1), dim3(256), 0, stream, a.groups, a.group_begin,
+                     a.device, a.P, kTileM, tiles, n_mtiles);
+  LLEP_CHECK_LAUNCH();
+  hipLaunchKernelGGL(wgrad_table_kernel, dim3(1), dim3(1024), 0, stream, a.groups, a.group_begin,
+                     a.device, a.P, a.E, a.E / a.P, kbase, gprow, chunk, wge, n_wg, kslices);
+  LLEP_CHECK_LAUNCH();
+  constexpr int NT = 64 * kWavesM * kWavesN;
+  constexpr int NT192 = 64 * kWavesM192 * kWavesN192;
+  const bool d192 = D % 256 != 0 && D % 192 == 0;
+  const bool f192 = F % 256 != 0 && F % 192 == 0;
+  // 1. g, u = X [Wg | Wu] (interleaved per 32), blocked over padded rows
+  GemmArgs g = {};
+  g.A = static_cast<const uint16_t *>(a.x_perm);
+  g.lda = D;
+  g.B = static_cast<const uint16_t *>(a.w_gate_up);
+  g.b_expert_stride = int64_t(2) * F * D;
+  g.b_blk_stride = int64_t(D / kSK) * 1024;
+  g.C = gu;
+  g.ldc = 2 * F;
+  g.groups = a.groups;
+  g.tiles = tiles;
+  g.n_mtiles = n_mtiles;
+  g.N = 2 * F;
+  g.Kdim = D;
+  hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, false, true>), dim3(grid),
+                     dim3(NT), 0, stream, g);
+  LLEP_CHECK_LAUNCH();
+  // 2. d act = d out Wd^T; epilogue writes d g, d u (into dgu) and act
+  GemmArgs g2 = g;
+  g2.A = static_cast<const uint16_t *>(a.d_out_perm);
+  g2.lda = D;
+  g2.B = static_cast<const uint16_t *>(a.w_down_t);
+  g2.b_expert_stride = int64_t(F) * D;
+  g2.b_blk_stride = int64_t(D / kSK) * 1024;
+  g2.C = dgu;
+  g2.ldc = F;
+  g2.N = F;
+  g2.Kdim = D;
+  g2.GU = gu;
+  g2.act = act;
+  if (f192)
+    hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiSwigluBwd, false, true>),
+                       dim3(grid), dim3(NT192), 0, stream, g2);
+  else
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiSwigluBwd, false, true>),
+                       dim3(grid), dim3(NT), 0, stream, g2);
+  LLEP_CHECK_LAUNCH();
+  // 3. dX = [d g | d u] [Wg | Wu]^T into the x_perm rows
+  GemmArgs g3 = g;
+  g3.A = dgu;
+  g3.lda = 2 * F;
+  g3.a_blk_stride = int64_t(2 * F / kSK) * 1024;
+  g3.B = static_cast<const uint16_t *>(a.w_gate_up_t);
+  g3.b_expert_stride = int64_t(2) * F * D;
+  g3.b_blk_stride = int64_t(2 * F / kSK) * 1024;
+  g3.C = static_cast<uint16_t *>(a.dx_perm);
+  g3.ldc = D;
+  g3.N = D;
+  g3.Kdim = 2 * F;
+  if (d192)
+    hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiPlain, true, false>),
+                       dim3(grid), dim3(NT192), 0, stream, g3);
+  else
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, true, false>), dim3(grid),
+                       dim3(NT), 0, stream, g3);
+  LLEP_CHECK_LAUNCH();
+  // 4. the weight-gradient operands, then the two weight-gradient GEMMs
+  const int tg = 4 * grid;
+  hipLaunchKernelGGL(to_wgrad_kernel<false>, dim3(tg), dim3(256), 0, stream,
+                     static_cast<const uint16_t *>(a.x_perm), int64_t(D), D, a.groups, a.device,
+                     a.group_begin, a.P, kbase, gprow, chunk, kslices, L.kmax, xt);
+  LLEP_CHECK_LAUNCH();
+  hipLaunchKernelGGL(to_wgrad_kernel<false>, dim3(tg), dim3(256), 0, stream,
+                     static_cast<const uint16_t *>(a.d_out_perm), int64_t(D), D, a.groups,
+                     a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices, L.kmax, dot);
+  LLEP_CHECK_LAUNCH();
+  hipLaunchKernelGGL(to_wgrad_kernel<true>, dim3(tg), dim3(256), 0, stream, act, int64_t(F), F,
+                     a.groups, a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices, L.kmax,
+                     actt);
+  LLEP_CHECK_LAUNCH();
+  hipLaunchKernelGGL(to_wgrad_kernel<true>, dim3(tg), dim3(256), 0, stream, dgu, int64_t(2 * F),
+                     2 * F, a.groups, a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices,
+                     L.kmax, dgut);
+  LLEP_CHECK_LAUNCH();
+  GemmArgs w1 = {};
+  w1.A = xt;
+  w1.a_blk_stride = (L.kmax / 32) * 1024;
+  w1.B = dgut;
+  w1.b_blk_stride = (L.kmax / 32) * 1024;
+  w1.M = D;
+  w1.N = 2 * F;
+  w1.wg_experts = wge;
+  w1.n_wg = n_wg;
+  w1.Cf = a.dw_gate;
+  w1.Cf2 = a.dw_up;
+  w1.cf_expert_stride = int64_t(D) * F;
+  hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiWgradGU, true, false>),
+                     dim3(grid), dim3(NT), 0, stream, w1);
+  LLEP_CHECK_LAUNCH();
+  GemmArgs w2 = w1;
+  w2.A = actt;
+  w2.B = dot;
+  w2.M = F;
+  w2.N = D;
+  w2.Cf = a.dw_down;
+  w2.Cf2 = nullptr;
+  w2.cf_expert_stride = int64_t(F) * D;
+  if (d192)
+    hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiWgradD, true, false>),
+                       dim3(grid), dim3(NT192), 0, stream, w2);
+  else
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiWgradD, true, false>),
+                       dim3(grid), dim3(NT), 0, stream, w2);
+  LLEP_CHECK_LAUNCH();
+#undef LLEP_CHECK_LAUNCH
+  return hipSuccess;
 }
 
 }  // namespace llep

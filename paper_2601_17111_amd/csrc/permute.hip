@@ -251,7 +251,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const i32x4 *__restrict__ 
         const int nk = min(kWave, K - kb);
         int32_t rv = lane < nk ? pair_row[t * K + kb + lane] : -1;
         if (rv >= R) rv = -1;
-        const float gv = lane < nk ? gates[t * K + kb + lane] : 0.0f;
+        const float gv = lane < nk ? (gates ? gates[t * K + kb + lane] : 1.0f) : 0.0f;
         for (int k0 = 0; k0 < nk; k0 += kPairs) {
           int32_t row[kPairs];
           float g[kPairs];
@@ -343,6 +343,115 @@ hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
     launch_combine_t<true>(stream, a, vecs);
   else
     launch_combine_t<false>(stream, a, vecs);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Backward of the combine (Eq. 1). For every valid pair (t, k) with row
+// r = pair_row[t*K + k]:
+//   d_out_perm[r] = gates[t, k] * dy[t]              (one rounding)
+//   d_gates[t, k] = sum_i dy[t, i] * out_perm[r, i]  (float32)
+// and d_gates = 0 for pairs without a row. One wavefront per token; the
+// token's dy slice is held in registers while the pairs' rows stream past.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+template <int kV>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(
+    const i32x4 *__restrict__ out_perm, const int32_t *__restrict__ pair_row,
+    const float *__restrict__ gates, const i32x4 *__restrict__ dy, i32x4 *__restrict__ d_out_perm,
+    float *__restrict__ d_gates, int64_t T, int32_t K, int32_t vecs) {
+  const int64_t R = T * K;
+  constexpr int kPairs = kCombinePairs;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = lane_id();
+  for (int64_t t = int64_t(blockIdx.x) * 4 + w; t < T; t += int64_t(gridDim.x) * 4) {
+    for (int kb = 0; kb < K; kb += kWave) {
+      const int nk = min(kWave, K - kb);
+      int32_t rv = lane < nk ? pair_row[t * K + kb + lane] : -1;
+      if (rv >= R) rv = -1;
+      const float gv = lane < nk ? gates[t * K + kb + lane] : 0.0f;
+      float dg = 0.0f;  // lane j: d gate of pair kb + j
+      for (int v0 = 0; v0 < vecs; v0 += kV * kWave) {
+        i32x4 dv[kV];
+#pragma unroll
+        for (int b = 0; b < kV; ++b) {
+          const int v = v0 + b * kWave + lane;
+          dv[b] = v < vecs ? dy[t * vecs + v] : i32x4{0, 0, 0, 0};
+        }
+        for (int k0 = 0; k0 < nk; k0 += kPairs) {
+          int32_t row[kPairs];
+          float g[kPairs];
+          i32x4 q[kPairs][kV];
+#pragma unroll
+          for (int j = 0; j < kPairs; ++j) {
+            row[j] = k0 + j < nk ? __builtin_amdgcn_readlane(rv, k0 + j) : -1;
+            g[j] = __int_as_float(
+                __builtin_amdgcn_readlane(__float_as_int(gv), k0 + j < nk ? k0 + j : 0));
+          }
+#pragma unroll
+          for (int j = 0; j < kPairs; ++j) {
+            if (row[j] < 0) continue;
+#pragma unroll
+            for (int b = 0; b < kV; ++b) {
+              const int v = v0 + b * kWave + lane;
+              q[j][b] = v < vecs ? out_perm[int64_t(row[j]) * vecs + v] : i32x4{0, 0, 0, 0};
+            }
+          }
+#pragma unroll
+          for (int j = 0; j < kPairs; ++j) {
+            if (row[j] < 0) continue;
+            float part = 0.0f;
+#pragma unroll
+            for (int b = 0; b < kV; ++b) {
+              const int v = v0 + b * kWave + lane;
+              i32x4 o;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const uint32_t du = uint32_t(dv[b][i]), qu = uint32_t(q[j][b][i]);
+                const float d0 = __uint_as_float(du << 16), d1 = __uint_as_float(du & 0xffff0000u);
+                part = fmaf(d0, __uint_as_float(qu << 16), part);
+                part = fmaf(d1, __uint_as_float(qu & 0xffff0000u), part);
+                o[i] = int32_t(uint32_t(f32_to_bf16(g[j] * d0)) |
+                               (uint32_t(f32_to_bf16(g[j] * d1)) << 16));
+              }
+              if (v < vecs) d_out_perm[int64_t(row[j]) * vecs + v] = o;
+            }
+            const float s = wave_sum(part);
+            if (lane == k0 + j) dg += s;
+          }
+        }
+      }
+      if (lane < nk) d_gates[t * K + kb + lane] = rv >= 0 ? dg : 0.0f;
+    }
+  }
+}
+
+template <int kV>
+void launch_combine_bwd_v(int grid, hipStream_t stream, const CombineBwdArgs &a, int32_t vecs) {
+  hipLaunchKernelGGL((combine_bwd_kernel<kV>), dim3(grid), dim3(256), 0, stream,
+                     static_cast<const i32x4 *>(a.out_perm), a.pair_row, a.gates,
+                     static_cast<const i32x4 *>(a.dy), static_cast<i32x4 *>(a.d_out_perm),
+                     a.d_gates, a.T, a.K, vecs);
+}
+
+hipError_t launch_combine_backward(const CombineBwdArgs &a, hipStream_t stream) {
+  if (a.T == 0) return hipSuccess;
+  const int32_t vecs = a.D / 8;  // bfloat16 rows
+  const int kv = vecs_per_lane(vecs, kCombineMaxVecs);
+  const int64_t blocks = (a.T + 3) / 4;
+  const int grid = int(blocks < 65536 ? blocks : 65536);
+  switch (kv) {
+    case 1: launch_combine_bwd_v<1>(grid, stream, a, vecs); break;
+    case 2: launch_combine_bwd_v<2>(grid, stream, a, vecs); break;
+    case 3: launch_combine_bwd_v<3>(grid, stream, a, vecs); break;
+    default: launch_combine_bwd_v<4>(grid, stream, a, vecs); break;
+  }
   return hipGetLastError();
 }
 

@@ -62,3 +62,37 @@ class LLEPLayer:
         self.ffn(w_gate_up, w_down, -1 if device is None else device, stream)
         self.combine(gates, stream)
         return self.y
+
+    def backward(self, dy, gates, w_gate_up, w_gate_up_t, w_down_t, device: int = -1,
+                 stream=None):
+        """Backward of forward() (bf16), reusing its plan, permutation and expert
+        outputs: combine backward -> grouped FFN backward (one device's groups,
+        or all with -1) -> the pairs' input gradients summed per token.
+
+        Returns (dx [T, D], d_gates [T, K] float32, dw_gate, dw_up [E, D, F],
+        dw_down [E, F, D] float32). dx and d_gates cover every token only when
+        device == -1; the weight gradients are the device's partials, or with
+        -1 the totals after the gradient return (experts without rows: zero).
+        """
+        import torch
+        if not hasattr(self, "d_out_perm"):
+            R = max(self.T * self.K, 1)
+            dev, E, D, F = self.device, self.E, self.D, self.F
+            self.d_out_perm = torch.empty((R, D), dtype=self.dtype, device=dev)
+            self.dx_perm = torch.empty((R, D), dtype=self.dtype, device=dev)
+            self.d_gates = torch.empty((self.T, self.K), dtype=torch.float32, device=dev)
+            self.dx = torch.empty((self.T, D), dtype=self.dtype, device=dev)
+            self.dw_gate = torch.empty((E, D, F), dtype=torch.float32, device=dev)
+            self.dw_up = torch.empty((E, D, F), dtype=torch.float32, device=dev)
+            self.dw_down = torch.empty((E, F, D), dtype=torch.float32, device=dev)
+            nbytes = B.llep_grouped_ffn_backward_workspace_bytes(self.params, D, F, B.LLEP_BF16)
+            self.bwd_workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        for w in (self.dw_gate, self.dw_up, self.dw_down):
+            w.zero_()
+        B.llep_combine_backward(self.params, self.out_perm, self.pair_row, gates, dy,
+                                self.d_out_perm, self.d_gates, stream)
+        B.llep_grouped_ffn_backward(self.params, self.bufs, device, self.x_perm, self.d_out_perm,
+                                    w_gate_up, w_gate_up_t, w_down_t, self.dx_perm, self.dw_gate,
+                                    self.dw_up, self.dw_down, self.bwd_workspace, stream)
+        B.llep_combine(self.params, self.dx_perm, self.pair_row, None, self.dx, stream)
+        return self.dx, self.d_gates, self.dw_gate, self.dw_up, self.dw_down

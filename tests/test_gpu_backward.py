@@ -1,0 +1,281 @@
+"""GPU parity of the backward pass against the oracle: the combine's backward
+exactly (up to float32 summation order), the layer's input, gate and weight
+gradients within the bf16 tolerance, the per-device partial weight gradients
+and the gradient return, and the edge cases."""
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import LayerRun, device, rel_err
+
+pytestmark = pytest.mark.gpu
+
+TOL_BF16 = 2e-2
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+def _cfg(name, alpha=(11, 10), routing=("hot", 0.7, 2), **shape):
+    from fractions import Fraction
+    from paper_2601_17111_amd.synth import LayerConfig
+    return LayerConfig(name, alpha=Fraction(*alpha), dtype="bf16", routing=routing, **shape)
+
+
+def _dy(cfg, seed, dev):
+    import torch
+    g = torch.Generator(device="cpu").manual_seed(1000 + seed)
+    return torch.randn(cfg.T, cfg.D, generator=g).to(torch.bfloat16).to(dev)
+
+
+class BwdRun(LayerRun):
+    def __init__(self, cfg, seed, dev, mode="llep"):
+        super().__init__(cfg, seed, dev, mode)
+        import torch
+        from paper_2601_17111_amd import binding as B
+        self.gut, self.dnt = B.llep_pack_weights_backward(self.wg, self.wu, self.wd)
+        self.dy = _dy(cfg, seed, dev)
+        torch.cuda.synchronize()
+
+    def backward(self, device=-1):
+        import torch
+        self.forward(-1)
+        out = self.layer.backward(self.dy, self.gates, self.gu, self.gut, self.dnt, device)
+        torch.cuda.synchronize()
+        return [t.float().cpu().numpy() for t in out]
+
+
+def test_pack_weights_backward_layout(dev):
+    """Every element of the backward packing sits where the header puts it."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    E, D, F = 2, 128, 192
+    g = torch.Generator(device="cpu").manual_seed(5)
+    wg, wu = (torch.randn(E, D, F, generator=g).to(torch.bfloat16) for _ in range(2))
+    wd = torch.randn(E, F, D, generator=g).to(torch.bfloat16)
+    gut, dnt = B.llep_pack_weights_backward(wg.to(dev), wu.to(dev), wd.to(dev))
+    torch.cuda.synchronize()
+    gut, dnt = gut.cpu().reshape(E, -1), dnt.cpu().reshape(E, -1)
+
+    def idx(n, k, K):
+        return ((n // 16) * (K // 32) + k // 32) * 512 + (n % 16) * 32 + k % 32
+
+    n = np.arange(D)[:, None]
+    k = np.arange(2 * F)[None, :]
+    col = 32 * (k // 64) + k % 32
+    for e in range(E):
+        want = torch.where(torch.from_numpy(np.broadcast_to(k % 64 < 32, (D, 2 * F))),
+                           wg[e][:, col[0]], wu[e][:, col[0]])
+        assert torch.equal(gut[e][torch.from_numpy(idx(n, k, 2 * F))], want)
+        nf = np.arange(F)[:, None]
+        kd = np.arange(D)[None, :]
+        assert torch.equal(dnt[e][torch.from_numpy(idx(nf, kd, D))], wd[e])
+
+
+def test_combine_backward_rows_and_gates(dev):
+    """d_out_perm = gate * dy with one rounding (bit-exact); d gates are the
+    dot products of dy with the expert rows the forward produced."""
+    import torch
+    cfg = _cfg("cb", T=613, D=192, F=128, E=8, K=3, P=4)
+    run = BwdRun(cfg, 2, dev)
+    run.backward(-1)
+    L = run.layer
+    pr = L.pair_row.cpu().numpy()[:cfg.T * cfg.K]
+    want_rows = (run.gates.reshape(-1, 1).cpu() * run.dy.float().cpu().repeat_interleave(cfg.K, 0)
+                 ).to(torch.bfloat16)
+    got_rows = L.d_out_perm.cpu()[torch.from_numpy(pr.astype(np.int64))]
+    assert torch.equal(got_rows, want_rows)
+    out = L.out_perm.float().cpu().numpy().astype(np.float64)[pr]
+    dy = run.dy.float().cpu().numpy().astype(np.float64)
+    want_g = np.einsum("pd,pd->p", np.repeat(dy, cfg.K, 0), out).reshape(cfg.T, cfg.K)
+    got_g = L.d_gates.cpu().numpy()
+    assert np.allclose(got_g, want_g, rtol=1e-5, atol=1e-5 * np.abs(want_g).max())
+
+
+@pytest.mark.parametrize("T,K,D", [(37, 70, 4096), (200, 5, 136), (3, 4, 8)])
+def test_combine_backward_standalone(dev, T, K, D):
+    """Rows longer than one wave slice, rows of a ragged number of vectors,
+    K > 64 (two 64-pair batches), and an invalid pair."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    E, P = 8, 2
+    rng = np.random.default_rng(9 + D)
+    ids = rng.integers(0, E, (T, K)).astype(np.int32)
+    ids[min(5, T - 1), 3] = E + 1  # an invalid pair: no row, d gate 0
+    params = B.make_params(T, K, E, P, T * K)
+    bufs = B.PlanBuffers(params, dev)
+    ids_t = torch.from_numpy(ids).to(dev)
+    gates = torch.from_numpy(rng.random((T, K)).astype(np.float32)).to(dev)
+    x = torch.randn(T, D, device=dev).to(torch.bfloat16)
+    R = T * K
+    x_perm = torch.empty(R, D, dtype=torch.bfloat16, device=dev)
+    gp = torch.empty(R, dtype=torch.float32, device=dev)
+    rp = torch.empty(R, dtype=torch.int32, device=dev)
+    pr = torch.empty(R, dtype=torch.int32, device=dev)
+    B.llep_plan(params, ids_t, bufs)
+    B.llep_permute(params, bufs, ids_t, gates, x, x_perm, gp, rp, pr)
+    out_perm = torch.randn(R, D, device=dev).to(torch.bfloat16)
+    dy = torch.randn(T, D, device=dev).to(torch.bfloat16)
+    d_out = torch.zeros(R, D, dtype=torch.bfloat16, device=dev)
+    dg = torch.full((T, K), 7.0, device=dev)
+    B.llep_combine_backward(params, out_perm, pr, gates, dy, d_out, dg)
+    torch.cuda.synchronize()
+    prn = pr.cpu().numpy()
+    bad = min(5, T - 1) * K + 3
+    assert prn[bad] == -1
+    valid = prn >= 0
+    o = out_perm.float().cpu().numpy().astype(np.float64)
+    d = dy.float().cpu().numpy().astype(np.float64)
+    want = np.zeros(R)
+    want[valid] = np.einsum("pd,pd->p", np.repeat(d, K, 0)[valid], o[prn[valid]])
+    got = dg.cpu().numpy().reshape(-1)
+    assert got[bad] == 0.0
+    assert np.allclose(got, want, rtol=1e-5, atol=1e-5 * np.abs(want).max())
+    g = gates.cpu().numpy().reshape(-1)
+    want_rows = (torch.from_numpy(g[valid]).reshape(-1, 1) *
+                 torch.from_numpy(np.repeat(d, K, 0)[valid]).float()).to(torch.bfloat16)
+    assert torch.equal(d_out.cpu()[torch.from_numpy(prn[valid].astype(np.int64))], want_rows)
+
+
+SHAPES = [
+    dict(T=1000, D=256, F=320, E=16, K=4, P=4),
+    dict(T=777, D=128, F=192, E=8, K=2, P=8),
+    dict(T=600, D=192, F=256, E=12, K=3, P=4),
+    dict(T=97, D=64, F=64, E=4, K=1, P=2),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"T{s['T']}D{s['D']}F{s['F']}E{s['E']}")
+@pytest.mark.parametrize("mode", ["llep", "ep"])
+def test_layer_backward_matches_oracle(dev, shape, mode):
+    """dx, d gates and the per-expert weight gradients (after the gradient
+    return) against the plan-free gradients of the oracle."""
+    cfg = _cfg("bwd", **shape)
+    run = BwdRun(cfg, 4, dev, mode)
+    dx, dgates, dwg, dwu, dwd = run.backward(-1)
+    W = run.host_weights(range(cfg.E))
+    dy = run.dy.float().cpu().numpy()
+    x = run.x.float().cpu().numpy()
+    want_dx, want_dg, want_dW = oracle.moe_backward(x, run.inp.ids, run.inp.gates,
+                                                    lambda e: W[e], dy, cfg.E)
+    assert rel_err(dx, want_dx) <= TOL_BF16
+    assert rel_err(dgates, want_dg) <= TOL_BF16
+    for e in range(cfg.E):
+        if e not in want_dW:
+            assert not dwg[e].any() and not dwu[e].any() and not dwd[e].any()
+            continue
+        for got, want in zip((dwg[e], dwu[e], dwd[e]), want_dW[e]):
+            assert rel_err(got, want) <= TOL_BF16, e
+
+
+def test_backward_llep_equals_ep_per_row(dev):
+    """The input and gate gradients are row-local: the LLEP and EP plans give
+    the same bits; the weight gradients agree up to summation order."""
+    cfg = _cfg("bwd-eq", T=900, D=128, F=192, E=8, K=4, P=4, routing=("hot", 0.8, 1))
+    a = BwdRun(cfg, 6, dev, "llep").backward(-1)
+    b = BwdRun(cfg, 6, dev, "ep").backward(-1)
+    assert np.array_equal(a[0], b[0])
+    assert np.array_equal(a[1], b[1])
+    for x, y in zip(a[2:], b[2:]):
+        assert rel_err(x, y) <= 1e-5
+
+
+def test_backward_device_partials_and_return(dev):
+    """Per device: its partial weight gradients equal the oracle's partials of
+    that device's groups, only its experts are written, only its rows of
+    dx_perm are written; the partials added in return order give the totals."""
+    import torch
+    cfg = _cfg("bwd-dev", T=1500, D=192, F=256, E=16, K=4, P=4, routing=("hot", 0.8, 1))
+    run = BwdRun(cfg, 1, dev)
+    tot = [t.copy() for t in run.backward(-1)[2:]]
+    L = run.layer
+    dx_perm_all = L.dx_perm.clone()
+    ids_flat = run.inp.ids.reshape(-1)
+    pl = oracle.plan(ids_flat.tolist(), cfg.E, cfg.P, cfg.capacity, cfg.min_chunk, lam=cfg.lam)
+    _, row_pair = oracle.permute(ids_flat.tolist(), pl, cfg.E)
+    W = run.host_weights(range(cfg.E))
+    x = run.x.float().cpu().numpy()
+    dy = run.dy.float().cpu().numpy()
+    _, partials, dW = oracle.plan_backward(x, ids_flat, run.inp.gates.reshape(-1), lambda e: W[e],
+                                           dy, pl, np.asarray(row_pair), cfg.K, cfg.E // cfg.P)
+    assert any(d != e // (cfg.E // cfg.P) for (d, e) in partials)  # something spilled
+    rows = L.bufs.device_rows.cpu().tolist()
+    starts = np.concatenate([[0], np.cumsum(rows)])
+    summed = {}
+    M = cfg.E // cfg.P
+    for d in range(cfg.P):
+        L.dx_perm.fill_(float("nan"))
+        parts = [t.copy() for t in run.backward(d)[2:]]
+        dxp = L.dx_perm[:int(starts[-1])]
+        a, b = int(starts[d]), int(starts[d + 1])
+        assert torch.equal(dxp[a:b], dx_perm_all[a:b])
+        mask = torch.ones(dxp.shape[0], dtype=torch.bool, device=dxp.device)
+        mask[a:b] = False
+        assert torch.isnan(dxp[mask].float()).all()
+        mine = {e for (dd, e) in partials if dd == d}
+        for e in range(cfg.E):
+            if e not in mine:
+                assert not any(p[e].any() for p in parts)
+                continue
+            for got, want in zip((p[e] for p in parts), partials[(d, e)]):
+                assert rel_err(got, want) <= TOL_BF16, (d, e)
+            summed.setdefault(e, []).append((d, [p[e].astype(np.float64) for p in parts]))
+    for e, lst in summed.items():
+        lst.sort(key=lambda t: (t[0] != e // M, t[0]))  # native first, then by device
+        acc = [np.zeros_like(q) for q in lst[0][1]]
+        for _, ps in lst:
+            acc = [u + v for u, v in zip(acc, ps)]
+        for s, t, want in zip(acc, (tot[0][e], tot[1][e], tot[2][e]), dW[e]):
+            assert rel_err(t, s) <= 1e-5, e
+            assert rel_err(t, want) <= TOL_BF16, e
+
+
+def test_backward_empty_and_single_rows(dev):
+    """T == 0 enqueues nothing; groups of one row (every expert hit once)."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    from paper_2601_17111_amd.layer import LLEPLayer
+    layer = LLEPLayer(0, 2, 8, 4, 64, 64, 1, torch.bfloat16, dev)
+    z = torch.zeros((8, 64, 64), dtype=torch.bfloat16, device=dev)
+    gu, dn = B.llep_pack_weights(z, z, z)
+    gut, dnt = B.llep_pack_weights_backward(z, z, z)
+    ids = torch.zeros((0, 2), dtype=torch.int32, device=dev)
+    gates = torch.zeros((0, 2), dtype=torch.float32, device=dev)
+    x = torch.zeros((0, 64), dtype=torch.bfloat16, device=dev)
+    layer.forward(ids, gates, x, gu, dn, -1)
+    out = layer.backward(torch.zeros((0, 64), dtype=torch.bfloat16, device=dev), gates, gu, gut,
+                         dnt, -1)
+    torch.cuda.synchronize()
+    assert out[0].shape == (0, 64)
+    assert not any(t.any() for t in out[2:])
+    # one pair per expert: groups of a single row
+    cfg = _cfg("bwd-one", T=8, D=64, F=128, E=8, K=1, P=2, routing=("hot", 0.0, 1))
+    run = BwdRun(cfg, 0, dev)
+    ids1 = np.arange(8, dtype=np.int32).reshape(8, 1)
+    run.inp.ids = ids1
+    run.ids = torch.from_numpy(ids1).to(dev)
+    dx, dgates, dwg, dwu, dwd = run.backward(-1)
+    W = run.host_weights(range(cfg.E))
+    want_dx, want_dg, want_dW = oracle.moe_backward(run.x.float().cpu().numpy(), ids1,
+                                                    run.inp.gates, lambda e: W[e],
+                                                    run.dy.float().cpu().numpy(), cfg.E)
+    assert rel_err(dx, want_dx) <= TOL_BF16
+    assert rel_err(dgates, want_dg) <= TOL_BF16
+    for e in range(cfg.E):
+        for got, want in zip((dwg[e], dwu[e], dwd[e]), want_dW[e]):
+            assert rel_err(got, want) <= TOL_BF16, e
+
+
+def test_backward_rejects_bad_arguments(dev):
+    import torch
+    from paper_2601_17111_amd import binding as B
+    params = B.make_params(16, 2, 8, 4, 8)
+    assert B.llep_grouped_ffn_backward_workspace_bytes(params, 64, 64, B.LLEP_F32) == 0
+    assert B.llep_grouped_ffn_backward_workspace_bytes(params, 64, 64, B.LLEP_BF16) > 0
+    z = torch.zeros((8, 64, 64), dtype=torch.float32, device=dev)
+    with pytest.raises(B.LLEPError) as ei:
+        B.llep_pack_weights_backward(z, z, z)
+    assert ei.value.code == B.LLEP_E_DTYPE
