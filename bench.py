@@ -45,6 +45,7 @@ def _parse():
     ap.add_argument("--cpu-sample-rows", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ep", action="store_true", help="skip the standard-EP comparison")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before warmup, run a plain 1 GiB -> 1 GiB elementwise copy (torch.neg on "
                          "float32) three times: a kernel of known traffic that scales the HBM "
@@ -120,6 +121,58 @@ def _time_steps(layer, run, steps, dstar):
         for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
             seg[k] += a.elapsed_time(b) / steps
     return wall * 1e3 / steps, seg
+
+
+def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps):
+    """The backward of the step on the most-loaded device's share: combine
+    backward (all tokens) -> grouped SwiGLU backward of d*'s groups (input
+    gradients of its rows and its partial weight gradients) -> the pairs'
+    input gradients summed per token. HIP event times per segment (ms)."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    gut, dnt = B.llep_pack_weights_backward(wg, wu, wd)
+    g = torch.Generator(device=run["x"].device)
+    g.manual_seed(7)
+    dy = torch.randn(cfg.T, cfg.D, generator=g, device=run["x"].device).to(torch.bfloat16)
+    layer.forward(run["ids"], run["gates"], run["x"], run["gu"], run["dn"], -1)
+    layer.backward(dy, run["gates"], run["gu"], gut, dnt, dstar)  # allocates the buffers
+    L = layer
+
+    def step():
+        B.llep_combine_backward(L.params, L.out_perm, L.pair_row, run["gates"], dy, L.d_out_perm,
+                                L.d_gates)
+        e[1].record()
+        B.llep_grouped_ffn_backward(L.params, L.bufs, dstar, L.x_perm, L.d_out_perm, run["gu"],
+                                    gut, dnt, L.dx_perm, L.dw_gate, L.dw_up, L.dw_down,
+                                    L.bwd_workspace)
+        e[2].record()
+        B.llep_combine(L.params, L.dx_perm, L.pair_row, None, L.dx)
+
+    seg = {"combine_backward": 0.0, "grouped_ffn_backward": 0.0, "dx_sum": 0.0}
+    for i in range(steps + 2):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record()
+        step()
+        e[3].record()
+        torch.cuda.synchronize()
+        if i >= 2:
+            for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
+                seg[k] += a.elapsed_time(b) / steps
+    D, F, T, K = cfg.D, cfg.F, cfg.T, cfg.K
+    R = T * K
+    t_ffn = seg["grouped_ffn_backward"] * 1e-3
+    cb_bytes = T * D * 2 + 2 * R * D * 2 + 12 * R
+    del gut, dnt
+    return {
+        "ms_per_step": sum(seg.values()), "segments_ms": seg, "device": dstar, "rows": n_rows,
+        # 12 D F per row: the backward of the three projections (twice the
+        # forward); 16 D F with the recomputed gate/up projection
+        "grouped_ffn_backward_TFLOPs": 12.0 * D * F * n_rows / t_ffn / 1e12,
+        "grouped_ffn_backward_executed_TFLOPs": 16.0 * D * F * n_rows / t_ffn / 1e12,
+        "grouped_ffn_backward_frac": 16.0 * D * F * n_rows / t_ffn / 1e12 / PEAK_BF16_TFLOPS,
+        "combine_backward_GBps": cb_bytes / (seg["combine_backward"] * 1e-3) / 1e9,
+        "tokens_per_s": T / (sum(seg.values()) * 1e-3),
+    }
 
 
 def _cpu_baseline(cfg, inp, expert_weights, args):
@@ -417,6 +470,10 @@ def main():
         "rows": total_rows,
         "grouped_ffn_TFLOPs": 6.0 * D * F * total_rows / (seg_full["grouped_ffn"] * 1e-3) / 1e12,
     }
+
+    if cfg.dtype == "bf16" and not args.no_backward:
+        out["backward"] = _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows,
+                                    max(3, args.steps // 2))
 
     if not args.no_ep:
         layer.set_mode("ep")

@@ -119,10 +119,22 @@ __global__ __launch_bounds__(256) void tile_table_kernel(const int32_t *__restri
 
 // Epilogues: the forward projections (plain bf16 C, or SwiGLU of gate/up
 // column pairs), the SwiGLU backward (C = d act; reads the recomputed gate /
-// up values, writes their gradients and the activation), and the two weight
-// gradients (fp32, per expert; gate/up columns de-interleaved).
-enum Epilogue : int { kEpiPlain = 0, kEpiSwiglu = 1, kEpiSwigluBwd = 2, kEpiWgradGU = 3,
-                      kEpiWgradD = 4 };
+// up values, writes their gradients and the activation), and the backward's
+// multi-problem launch: the input-gradient tiles (plain bf16 C) together with
+// the tiles of the two weight gradients (fp32, per expert; gate/up columns
+// de-interleaved), handed out through a work counter.
+enum Epilogue : int { kEpiPlain = 0, kEpiSwiglu = 1, kEpiSwigluBwd = 2, kEpiBwdMulti = 3 };
+
+// A weight-gradient problem: per expert e, C_e[m][n] = sum over the k-segment
+// of e of A[m][k] B[n][k], both operands blocked over the whole k range.
+struct WgProblem {
+  const uint16_t *A, *B;  // blocked [M][kmax], [N][kmax]
+  int64_t blk_stride;     // bytes per 16-row block of A and B (kmax / 32 KB)
+  float *C, *C2;          // C [E][M][N] fp32; gate/up problem: gate into C, up into C2,
+                          // each [E][M][N / 2]
+  int64_t expert_stride;  // elements per expert of C (and C2)
+  int32_t M, N, gate_up;
+};
 
 struct GemmArgs {
   const uint16_t *A;
@@ -140,12 +152,14 @@ struct GemmArgs {
   // SwiGLU backward
   const uint16_t *GU;  // blocked [padded rows][2F]: gate / up values
   uint16_t *act;       // blocked [padded rows][F]
-  // weight gradients: C is M x N per expert (fp32), over a k-segment per expert
-  int32_t M;
+  // multi-problem backward launch: weight-gradient tiles of the experts in
+  // wg_experts (longest k-segment first), problem wp[0] then wp[1] per
+  // expert, then the tiles of the main problem; tiles past the first gridDim
+  // come from the counter *queue (zero before the launch)
+  WgProblem wp[2];
   const int4 *wg_experts;  // (expert, first k-slice, k-slices, 0)
   const int32_t *n_wg;
-  float *Cf, *Cf2;         // dW (gate part / down) and the up part
-  int64_t cf_expert_stride;
+  int32_t *queue;
 };
 
 
@@ -234,6 +248,7 @@ __device__ __forceinline__ int lds_swz32(int row, int kc) {
 
 struct TileCoord {
   int e, row0, prow0, m0, rows_valid, n0, cols_valid, k0, nk;
+  int p, N;  // problem (0: the main one, 1 / 2: wp[0] / wp[1]) and its columns
 };
 
 template <int BM, int BN>
@@ -255,27 +270,36 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, 
   t.cols_valid = min(BN, g.N - t.n0);
   t.k0 = 0;
   t.nk = g.Kdim / kSK;
+  t.p = 0;
+  t.N = g.N;
   return true;
 }
 
-// weight-gradient tiles: (expert, m-tile, n-tile) over M x N, expert-major;
-// the contraction runs over the expert's k-segment
+// weight-gradient tile u < n_exp * (tiles of wp[0] + tiles of wp[1]):
+// expert-major, then problem, then m-tile, then n-tile; the contraction runs
+// over the expert's k-segment
 template <int BM, int BN>
-__device__ __forceinline__ bool decode_tile_wg(const GemmArgs &g, int u, int n_exp, TileCoord &t) {
-  const int n_mt = (g.M + BM - 1) / BM, n_nt = (g.N + BN - 1) / BN;
-  if (u >= n_exp * n_mt * n_nt) return false;
-  const int i = u / (n_mt * n_nt), rem = u - i * (n_mt * n_nt);
+__device__ __forceinline__ void decode_tile_wg(const GemmArgs &g, int u, int per0, int per1,
+                                               TileCoord &t) {
+  const int i = u / (per0 + per1);
+  int rem = u - i * (per0 + per1);
+  const bool second = rem >= per0;
+  rem -= second ? per0 : 0;
+  const int M = second ? g.wp[1].M : g.wp[0].M;
+  const int N = second ? g.wp[1].N : g.wp[0].N;
+  const int n_nt = (N + BN - 1) / BN;
   const int4 we = g.wg_experts[i];
   t.e = we.x;
   t.row0 = 0;
   t.prow0 = 0;
   t.m0 = (rem / n_nt) * BM;
-  t.rows_valid = min(BM, g.M - t.m0);
+  t.rows_valid = min(BM, M - t.m0);
   t.n0 = (rem % n_nt) * BN;
-  t.cols_valid = min(BN, g.N - t.n0);
+  t.cols_valid = min(BN, N - t.n0);
   t.k0 = we.y;
   t.nk = we.z;
-  return true;
+  t.p = second ? 2 : 1;
+  t.N = N;
 }
 
 // A is row-major (lda) or, with kABlocked, in 16 x 32 blocks over padded
@@ -289,7 +313,7 @@ void gemm256_kernel(GemmArgs g) {
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr bool kSwiglu = kEpi == kEpiSwiglu;
-  constexpr bool kWgrad = kEpi == kEpiWgradGU || kEpi == kEpiWgradD;
+  constexpr bool kMulti = kEpi == kEpiBwdMulti;
   // DMA blocks (16 rows each) per stage, dealt round-robin over the waves:
   // every wave has A_PER_WAVE A blocks and B_FULL B blocks, the first B_REM
   // waves one B block more. Waits count the PER_STAGE instructions every
@@ -320,14 +344,24 @@ void gemm256_kernel(GemmArgs g) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const int n_mt = kWgrad ? 0 : *g.n_mtiles;
-  const int n_exp = kWgrad ? *g.n_wg : 0;
+  const int n_mt = *g.n_mtiles;
   const int n_nt = (g.N + BN - 1) / BN;
+  int per0 = 0, per1 = 0, n_wgt = 0;
+  if constexpr (kMulti) {
+    per0 = ((g.wp[0].M + BM - 1) / BM) * ((g.wp[0].N + BN - 1) / BN);
+    per1 = ((g.wp[1].M + BM - 1) / BM) * ((g.wp[1].N + BN - 1) / BN);
+    n_wgt = *g.n_wg * (per0 + per1);
+  }
   const int G = gridDim.x;  // a multiple of 8
   const int slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
   auto decode = [&](int u, TileCoord &c) {
-    return kWgrad ? decode_tile_wg<BM, BN>(g, u, n_exp, c) : decode_tile<BM, BN>(g, u, n_mt, n_nt, c);
+    if (kMulti && u < n_wgt) {
+      decode_tile_wg<BM, BN>(g, u, per0, per1, c);
+      return true;
+    }
+    return decode_tile<BM, BN>(g, u - n_wgt, n_mt, n_nt, c);
   };
+  __shared__ int32_t s_next;  // multi-problem launch: the next tile from the counter
   const int kc_load = (lane & 3) ^ ((lane >> 4) & 3);
   const int64_t lda_b = g.lda * 2;
   // a 16 x 32 block is 1 KB; lane l fills LDS bytes 16l .. 16l+15 = row
@@ -340,17 +374,26 @@ void gemm256_kernel(GemmArgs g) {
   const char *Ab, *Bb;
   int32_t offA[A_PER_WAVE], offB[B_SLOTS];
   auto setup = [&](const TileCoord &c) {
+    const uint16_t *Ap = g.A, *Bp = g.B;
+    int64_t a_bs = g.a_blk_stride, b_es = g.b_expert_stride, b_bs = g.b_blk_stride;
+    if (kMulti && c.p != 0) {
+      const bool second = c.p == 2;
+      Ap = second ? g.wp[1].A : g.wp[0].A;
+      Bp = second ? g.wp[1].B : g.wp[0].B;
+      a_bs = b_bs = second ? g.wp[1].blk_stride : g.wp[0].blk_stride;
+      b_es = 0;
+    }
     // rows (columns) past the tile's valid ones re-read its last valid row
     // (block), so every address stays in bounds
     if (kABlocked) {
-      // forward: padded rows of the group; weight gradients: rows of the
-      // expert's M x K operand, from its k-segment on
-      const int64_t rb0 = kWgrad ? (c.m0 >> 4) : ((c.prow0 + c.m0) >> 4);
-      Ab = reinterpret_cast<const char *>(g.A) + rb0 * g.a_blk_stride + int64_t(c.k0) * 1024;
+      // padded rows of the group; weight gradients: rows of the expert's
+      // M x K operand (prow0 = 0), from its k-segment on
+      const int64_t rb0 = (c.prow0 + c.m0) >> 4;
+      Ab = reinterpret_cast<const char *>(Ap) + rb0 * a_bs + int64_t(c.k0) * 1024;
 #pragma unroll
       for (int j = 0; j < A_PER_WAVE; ++j) {
         const int rb = min(wave + NWD * j, (c.rows_valid - 1) >> 4);
-        offA[j] = int32_t(rb * g.a_blk_stride + blk_lane);
+        offA[j] = int32_t(rb * a_bs + blk_lane);
       }
     } else {
       Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
@@ -360,12 +403,12 @@ void gemm256_kernel(GemmArgs g) {
         offA[j] = int32_t(r * lda_b + kc_load * 16);
       }
     }
-    Bb = reinterpret_cast<const char *>(g.B) + int64_t(c.e) * g.b_expert_stride * 2 +
-         (c.n0 >> 4) * g.b_blk_stride + int64_t(c.k0) * 1024;
+    Bb = reinterpret_cast<const char *>(Bp) + int64_t(c.e) * b_es * 2 + (c.n0 >> 4) * b_bs +
+         int64_t(c.k0) * 1024;
 #pragma unroll
     for (int j = 0; j < B_SLOTS; ++j) {
       const int nb = min(wave + NWD * j, (c.cols_valid - 1) >> 4);
-      offB[j] = int32_t(nb * g.b_blk_stride + blk_lane);
+      offB[j] = int32_t(nb * b_bs + blk_lane);
     }
   };
   // request slice kt into stage st: 64 B per row along K for a row-major A,
@@ -469,6 +512,9 @@ void gemm256_kernel(GemmArgs g) {
 
   for (int it = 0;; ++it) {
     const int nk = t.nk;
+    // the tile after this one (read after the barrier that ends the loop;
+    // rewritten only after the barrier that ends the epilogue)
+    if (kMulti && threadIdx.x == 0) s_next = atomicAdd(g.queue, 1) + G;
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -522,7 +568,7 @@ void gemm256_kernel(GemmArgs g) {
     // every wave is done with the ring before the next tile's slices land
     __syncthreads();
     const TileCoord c = t;
-    const bool more = decode((it + 1) * G + slot, t);
+    const bool more = decode(kMulti ? s_next : (it + 1) * G + slot, t);
     // the next tile's first kAhead - 1 slices load during the epilogue; the
     // last stages hold the epilogue's staging area until the barrier below
     static_assert(kStages - (kAhead - 1) >= 2, "two stages free for staging");
@@ -659,63 +705,79 @@ void gemm256_kernel(GemmArgs g) {
           }
         }
       }
-    } else if constexpr (kWgrad) {
-      // fp32 weight gradient of expert c.e: C[m][n], rows m < M, written as
-      // 16-byte runs of 4 columns. Gate/up mode: column n = 64 q + cc is
-      // gate column 32 q + cc (cc < 32) or up column 32 q + cc - 32.
+    } else {
+      // fp32 weight gradient of expert c.e (problem c.p): C[m][n], rows
+      // m < M, written as 16-byte runs of 4 columns. Gate/up problem: column
+      // n = 64 q + cc is gate column 32 q + cc (cc < 32) or up column
+      // 32 q + cc - 32.
+      auto wgrad_epilogue = [&]() {
+        const bool second = c.p == 2;
+        float *C = second ? g.wp[1].C : g.wp[0].C;
+        float *C2 = g.wp[0].C2;
+        const bool gate_up = !second && g.wp[0].gate_up;
+        const int64_t es = second ? g.wp[1].expert_stride : g.wp[0].expert_stride;
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int m = c.m0 + wm * WM + i * 32 + (lane & 31);
-        if (i * 32 >= rows_w) break;
-        if (i * 32 + (lane & 31) >= rows_w) continue;
+        for (int i = 0; i < TM; ++i) {
+          const int m = c.m0 + wm * WM + i * 32 + (lane & 31);
+          if (i * 32 >= rows_w) break;
+          if (i * 32 + (lane & 31) >= rows_w) continue;
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col0 = c.n0 + wn * WN + j * 32;
-          if (col0 >= g.N) continue;
+          for (int j = 0; j < TN; ++j) {
+            const int col0 = c.n0 + wn * WN + j * 32;
+            if (col0 >= c.N) continue;
 #pragma unroll
-          for (int gq = 0; gq < 4; ++gq) {
-            const int n = col0 + 8 * gq + 4 * h;
-            float *dst;
-            if (kEpi == kEpiWgradGU) {
-              const int q = n >> 6, cc = n & 63;
-              const int Fo = g.N >> 1;
-              dst = (cc < 32 ? g.Cf : g.Cf2) + int64_t(c.e) * g.cf_expert_stride + int64_t(m) * Fo +
-                    32 * q + (cc & 31);
-            } else {
-              dst = g.Cf + int64_t(c.e) * g.cf_expert_stride + int64_t(m) * g.N + n;
+            for (int gq = 0; gq < 4; ++gq) {
+              const int n = col0 + 8 * gq + 4 * h;
+              float *dst;
+              if (gate_up) {
+                const int q = n >> 6, cc = n & 63;
+                dst = (cc < 32 ? C : C2) + int64_t(c.e) * es + int64_t(m) * (c.N >> 1) + 32 * q +
+                      (cc & 31);
+              } else {
+                dst = C + int64_t(c.e) * es + int64_t(m) * c.N + n;
+              }
+              *reinterpret_cast<f32x4 *>(dst) = f32x4{acc[i][j][4 * gq], acc[i][j][4 * gq + 1],
+                                                      acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]};
             }
-            *reinterpret_cast<f32x4 *>(dst) = f32x4{acc[i][j][4 * gq], acc[i][j][4 * gq + 1],
-                                                    acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]};
           }
         }
-      }
-    } else {
+      };
       // row-major C: 32 rows x WN columns per piece, rows RS bytes apart
-      static_assert(!kCBlocked, "blocked C: other epilogues");
-      constexpr int RS = WN * 2;
-      constexpr int CH = WN / 8;  // 16-byte chunks per row segment
-      static_assert(32 * RS <= STAGING, "staging");
-      const int ncol0 = c.n0 + wn * WN;
+      auto rowmajor_epilogue = [&]() {
+        static_assert(!kCBlocked, "blocked C: other epilogues");
+        constexpr int RS = WN * 2;
+        constexpr int CH = WN / 8;  // 16-byte chunks per row segment
+        static_assert(32 * RS <= STAGING, "staging");
+        const int ncol0 = c.n0 + wn * WN;
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        if (i * 32 >= rows_w) break;
+        for (int i = 0; i < TM; ++i) {
+          if (i * 32 >= rows_w) break;
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+          for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int gq = 0; gq < 4; ++gq)
-            *reinterpret_cast<uint2 *>(stg + (lane & 31) * RS + (j * 32 + 8 * gq + 4 * h) * 2) =
-                make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
-                           pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
-        char *crow = reinterpret_cast<char *>(
-            g.C + int64_t(c.row0 + c.m0 + wm * WM + i * 32) * g.ldc + ncol0);
+            for (int gq = 0; gq < 4; ++gq)
+              *reinterpret_cast<uint2 *>(stg + (lane & 31) * RS + (j * 32 + 8 * gq + 4 * h) * 2) =
+                  make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
+                             pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
+          char *crow = reinterpret_cast<char *>(
+              g.C + int64_t(c.row0 + c.m0 + wm * WM + i * 32) * g.ldc + ncol0);
 #pragma unroll
-        for (int r0 = 0; r0 < 32 * CH; r0 += kWave) {
-          const int q = r0 + lane;
-          const int row = q / CH, ch = q % CH;
-          if (q < 32 * CH && i * 32 + row < rows_w && ncol0 + ch * 8 < g.N)
-            *reinterpret_cast<i32x4 *>(crow + int64_t(row) * g.ldc * 2 + ch * 16) =
-                *reinterpret_cast<const i32x4 *>(stg + row * RS + ch * 16);
+          for (int r0 = 0; r0 < 32 * CH; r0 += kWave) {
+            const int q = r0 + lane;
+            const int row = q / CH, ch = q % CH;
+            if (q < 32 * CH && i * 32 + row < rows_w && ncol0 + ch * 8 < g.N)
+              *reinterpret_cast<i32x4 *>(crow + int64_t(row) * g.ldc * 2 + ch * 16) =
+                  *reinterpret_cast<const i32x4 *>(stg + row * RS + ch * 16);
+          }
         }
+      };
+      if constexpr (kMulti) {
+        if (c.p != 0)
+          wgrad_epilogue();
+        else
+          rowmajor_epilogue();
+      } else {
+        rowmajor_epilogue();
       }
     }
     if (more) {
@@ -987,14 +1049,17 @@ size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, 
 // weight-gradient row (kbase, a multiple of 32) in gradient-return order, its
 // first padded forward row (gprow, rows rounded to 16 per group, as the
 // tile list lays them out), the owner group of every 32-row chunk, and the
-// experts present with their segment (first 32-row slice, slices).
+// experts present with their segment (first 32-row slice, slices), longest
+// segment first (ties: lower expert id), so the work counter of the
+// multi-problem launch hands out the longest tiles first. Zeroes that
+// counter.
 __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
     int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase, int32_t *__restrict__ gprow,
     int32_t *__restrict__ chunk_group, int4 *__restrict__ wg_experts, int32_t *__restrict__ n_wg,
-    int32_t *__restrict__ kslices) {
+    int32_t *__restrict__ kslices, int32_t *__restrict__ queue) {
   __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks], s16[kMaxChunks];
-  __shared__ int32_t present[LLEP_MAX_EXPERTS];
+  __shared__ int32_t esl[LLEP_MAX_EXPERTS];
   const int tid = threadIdx.x;
   const int lo = device < 0 ? group_begin[0] : group_begin[device];
   const int hi = device < 0 ? group_begin[P] : group_begin[device + 1];
@@ -1021,25 +1086,24 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
   for (int e = tid; e < E; e += blockDim.x) {
     int32_t sl = 0;
     for (int j = 0; j < G; ++j) sl += se[j] == e ? ssl[j] : 0;
-    present[e] = sl > 0;
+    esl[e] = sl;
   }
   __syncthreads();
   for (int e = tid; e < E; e += blockDim.x) {
-    if (!present[e]) continue;
-    int32_t idx = 0, start = 0, sl = 0;
-    for (int f = 0; f < e; ++f) idx += present[f];
-    for (int j = 0; j < G; ++j) {
-      start += se[j] < e ? ssl[j] : 0;
-      sl += se[j] == e ? ssl[j] : 0;
-    }
+    const int32_t sl = esl[e];
+    if (sl == 0) continue;
+    int32_t idx = 0, start = 0;
+    for (int f = 0; f < E; ++f) idx += esl[f] > sl || (esl[f] == sl && f < e);
+    for (int j = 0; j < G; ++j) start += se[j] < e ? ssl[j] : 0;
     wg_experts[idx] = make_int4(e, start, sl, 0);
   }
   if (tid == 0) {
     int32_t n = 0, tot = 0;
-    for (int e = 0; e < E; ++e) n += present[e];
+    for (int e = 0; e < E; ++e) n += esl[e] > 0;
     for (int j = 0; j < G; ++j) tot += ssl[j];
     *n_wg = n;
     *kslices = tot;
+    *queue = 0;
   }
 }
 
@@ -1133,6 +1197,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   int32_t *n_mtiles = reinterpret_cast<int32_t *>(ws);
   int32_t *n_wg = n_mtiles + 1;
   int32_t *kslices = n_mtiles + 2;
+  int32_t *queue = n_mtiles + 3;
   int4 *tiles = reinterpret_cast<int4 *>(ws + L.tiles_off);
   int4 *wge = reinterpret_cast<int4 *>(ws + L.wge_off);
   int32_t *kbase = reinterpret_cast<int32_t *>(ws + L.kbase_off);
@@ -1157,7 +1222,8 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
                      a.device, a.P, kTileM, tiles, n_mtiles);
   LLEP_CHECK_LAUNCH();
   hipLaunchKernelGGL(wgrad_table_kernel, dim3(1), dim3(1024), 0, stream, a.groups, a.group_begin,
-                     a.device, a.P, a.E, a.E / a.P, kbase, gprow, chunk, wge, n_wg, kslices);
+                     a.device, a.P, a.E, a.E / a.P, kbase, gprow, chunk, wge, n_wg, kslices,
+                     queue);
   LLEP_CHECK_LAUNCH();
   constexpr int NT = 64 * kWavesM * kWavesN;
   constexpr int NT192 = 64 * kWavesM192 * kWavesN192;
@@ -1200,26 +1266,8 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
     hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiSwigluBwd, false, true>),
                        dim3(grid), dim3(NT), 0, stream, g2);
   LLEP_CHECK_LAUNCH();
-  // 3. dX = [d g | d u] [Wg | Wu]^T into the x_perm rows
-  GemmArgs g3 = g;
-  g3.A = dgu;
-  g3.lda = 2 * F;
-  g3.a_blk_stride = int64_t(2 * F / kSK) * 1024;
-  g3.B = static_cast<const uint16_t *>(a.w_gate_up_t);
-  g3.b_expert_stride = int64_t(2) * F * D;
-  g3.b_blk_stride = int64_t(2 * F / kSK) * 1024;
-  g3.C = static_cast<uint16_t *>(a.dx_perm);
-  g3.ldc = D;
-  g3.N = D;
-  g3.Kdim = 2 * F;
-  if (d192)
-    hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiPlain, true, false>),
-                       dim3(grid), dim3(NT192), 0, stream, g3);
-  else
-    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, true, false>), dim3(grid),
-                       dim3(NT), 0, stream, g3);
-  LLEP_CHECK_LAUNCH();
-  // 4. the weight-gradient operands, then the two weight-gradient GEMMs
+  // 3. the weight-gradient operands: X, d out, act and [d g | d u] with the
+  // rows of each expert laid end to end along k (gradient-return order)
   const int tg = 4 * grid;
   hipLaunchKernelGGL(to_wgrad_kernel<false>, dim3(tg), dim3(256), 0, stream,
                      static_cast<const uint16_t *>(a.x_perm), int64_t(D), D, a.groups, a.device,
@@ -1237,35 +1285,30 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
                      2 * F, a.groups, a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices,
                      L.kmax, dgut);
   LLEP_CHECK_LAUNCH();
-  GemmArgs w1 = {};
-  w1.A = xt;
-  w1.a_blk_stride = (L.kmax / 32) * 1024;
-  w1.B = dgut;
-  w1.b_blk_stride = (L.kmax / 32) * 1024;
-  w1.M = D;
-  w1.N = 2 * F;
-  w1.wg_experts = wge;
-  w1.n_wg = n_wg;
-  w1.Cf = a.dw_gate;
-  w1.Cf2 = a.dw_up;
-  w1.cf_expert_stride = int64_t(D) * F;
-  hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiWgradGU, true, false>),
-                     dim3(grid), dim3(NT), 0, stream, w1);
-  LLEP_CHECK_LAUNCH();
-  GemmArgs w2 = w1;
-  w2.A = actt;
-  w2.B = dot;
-  w2.M = F;
-  w2.N = D;
-  w2.Cf = a.dw_down;
-  w2.Cf2 = nullptr;
-  w2.cf_expert_stride = int64_t(F) * D;
-  if (d192)
-    hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiWgradD, true, false>),
-                       dim3(grid), dim3(NT192), 0, stream, w2);
-  else
-    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiWgradD, true, false>),
-                       dim3(grid), dim3(NT), 0, stream, w2);
+  // 4. one launch: dX = [d g | d u] [Wg | Wu]^T into the x_perm rows, and
+  // the weight gradients X^T [d g | d u] (de-interleaved into dWg, dWu) and
+  // act^T d out, per expert over its k-segment
+  GemmArgs g3 = g;
+  g3.A = dgu;
+  g3.lda = 2 * F;
+  g3.a_blk_stride = int64_t(2 * F / kSK) * 1024;
+  g3.B = static_cast<const uint16_t *>(a.w_gate_up_t);
+  g3.b_expert_stride = int64_t(2) * F * D;
+  g3.b_blk_stride = int64_t(2 * F / kSK) * 1024;
+  g3.C = static_cast<uint16_t *>(a.dx_perm);
+  g3.ldc = D;
+  g3.N = D;
+  g3.Kdim = 2 * F;
+  const int64_t wblk = (L.kmax / 32) * 1024;
+  g3.wp[0] = WgProblem{xt, dgut, wblk, a.dw_gate, a.dw_up, int64_t(D) * F, D, 2 * F, 1};
+  g3.wp[1] = WgProblem{actt, dot, wblk, a.dw_down, nullptr, int64_t(F) * D, F, D, 0};
+  g3.wg_experts = wge;
+  g3.n_wg = n_wg;
+  g3.queue = queue;
+  // 256 x 192 tiles: the 256 x 256 ring fills the LDS and leaves no room for
+  // the work counter's broadcast slot
+  hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiBwdMulti, true, false>),
+                     dim3(grid), dim3(NT192), 0, stream, g3);
   LLEP_CHECK_LAUNCH();
 #undef LLEP_CHECK_LAUNCH
   return hipSuccess;

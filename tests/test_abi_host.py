@@ -153,6 +153,46 @@ def test_ffn_argument_checks():
     assert L.llep_pack_weights(4, 64, 64, B.LLEP_BF16, a, None, a, a, a, None) == B.LLEP_E_ARG
 
 
+def test_backward_argument_checks():
+    L = _lib()
+    p = _params()
+    bufs = B.llep_plan_buffers(*[16 * (i + 1) for i in range(10)])
+    a = ctypes.c_void_p(4096)
+    bf = B.LLEP_BF16
+    # combine backward: bf16 only, nulls, alignment, D % 8
+    assert L.llep_combine_backward(ctypes.byref(p), a, a, a, a, 64, B.LLEP_F32, a, a,
+                                   None) == B.LLEP_E_DTYPE
+    assert L.llep_combine_backward(ctypes.byref(p), a, a, None, a, 64, bf, a, a,
+                                   None) == B.LLEP_E_ARG
+    assert L.llep_combine_backward(ctypes.byref(p), a, a, a, ctypes.c_void_p(4104), 64, bf, a, a,
+                                   None) == B.LLEP_E_ARG
+    assert L.llep_combine_backward(ctypes.byref(p), a, a, a, a, 60, bf, a, a, None) == B.LLEP_E_ARG
+    # the forward combine accepts null gates (all ones) but not a null output
+    assert L.llep_combine(ctypes.byref(p), a, a, None, 64, bf, None, None) == B.LLEP_E_ARG
+    # backward packing
+    assert L.llep_pack_weights_backward(4, 64, 64, B.LLEP_F32, a, a, a, a, a, None) == B.LLEP_E_DTYPE
+    assert L.llep_pack_weights_backward(4, 64, 96, bf, a, a, a, a, a, None) == B.LLEP_E_ARG
+    assert L.llep_pack_weights_backward(4, 64, 64, bf, a, a, a, None, a, None) == B.LLEP_E_ARG
+    # grouped FFN backward
+    assert B.llep_grouped_ffn_backward_workspace_bytes(p, 64, 128, B.LLEP_F32) == 0
+    need = B.llep_grouped_ffn_backward_workspace_bytes(p, 64, 128, bf)
+    # at least the recomputed gate/up values, their gradients and the activation
+    assert need >= p.T * p.K * 128 * 2 * 5
+    ws = ctypes.c_void_p(1 << 24)
+    ok = dict(device=0, D=64, F=128, dtype=bf, ws=ws, nbytes=need, dw=a)
+
+    def call(device, D, F, dtype, ws, nbytes, dw):
+        return L.llep_grouped_ffn_backward(ctypes.byref(p), ctypes.byref(bufs), device, a, a, a, a,
+                                           a, D, F, dtype, a, dw, a, a, ws, nbytes, None)
+    assert call(**dict(ok, dtype=B.LLEP_F32)) == B.LLEP_E_DTYPE
+    assert call(**dict(ok, D=96)) == B.LLEP_E_ARG
+    assert call(**dict(ok, device=4)) == B.LLEP_E_ARG
+    assert call(**dict(ok, dw=None)) == B.LLEP_E_ARG
+    assert call(**dict(ok, dw=ctypes.c_void_p(4100))) == B.LLEP_E_ARG
+    assert call(**dict(ok, nbytes=need - 1)) == B.LLEP_E_WORKSPACE
+    assert call(**dict(ok, ws=ctypes.c_void_p((1 << 24) + 64))) == B.LLEP_E_WORKSPACE
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "_lib", None)
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
