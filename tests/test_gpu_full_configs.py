@@ -183,3 +183,92 @@ def test_full_ep_equals_llep_bitwise(dev):
     y_ep = run.forward(-1)
     import torch
     assert torch.equal(y_llep, y_ep)
+
+
+BWD_CASES = ["gpt-oss-120b-hot1", "qwen3-30b-a3b", "deepseek-v3"]
+
+
+@pytest.mark.parametrize("name", BWD_CASES)
+def test_full_backward(dev, name):
+    """Backward at full size: weight-gradient columns of sampled experts (the
+    hot, spilled expert included) and input / gate gradients of sampled
+    tokens against float64 gradients computed from the inputs; every
+    device's partials summed in return order give the totals; under EP the
+    input and gate gradients are the same bits."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    cfg = _cfg(name)
+    run = LayerRun(cfg, 0, dev)
+    gut, dnt = B.llep_pack_weights_backward(run.wg, run.wu, run.wd)
+    g = torch.Generator(device="cpu").manual_seed(11)
+    dy_t = torch.randn(cfg.T, cfg.D, generator=g).to(torch.bfloat16)
+    dy_dev = dy_t.to(dev)
+    L = run.layer
+    run.forward(-1)
+    dx, dg, dwg, dwu, dwd = (t.clone() for t in L.backward(dy_dev, run.gates, run.gu, gut, dnt,
+                                                          -1))
+    torch.cuda.synchronize()
+    assert L.bufs.info_dict()["n_xfers"] > 0 or name != "gpt-oss-120b-hot1"
+    rng = np.random.default_rng(5)
+    ids, gates = run.inp.ids, run.inp.gates
+    S = _expert_subset(cfg, ids, 4, rng)
+    W = run.host_weights(S)
+    x = run.x.float().cpu().numpy().astype(np.float64)
+    dy = dy_t.float().numpy().astype(np.float64)
+    flat = ids.reshape(-1)
+    # weight-gradient columns: all rows of expert e, plan-free
+    for e in S:
+        pairs = np.nonzero(flat == e)[0]
+        if len(pairs) == 0:
+            assert not dwg[e].any()
+            continue
+        wg, wu, wd = (w.astype(np.float64) for w in W[e])
+        X = x[pairs // cfg.K]
+        dO = gates.reshape(-1)[pairs, None].astype(np.float64) * dy[pairs // cfg.K]
+        for f in rng.choice(cfg.F, size=2, replace=False):
+            gc, uc = X @ wg[:, f], X @ wu[:, f]
+            da = dO @ wd[f, :]
+            s = 1.0 / (1.0 + np.exp(-gc))
+            dgc = da * uc * s * (1 + gc * (1 - s))
+            duc = da * gc * s
+            for got, want in ((dwg[e][:, f], X.T @ dgc), (dwu[e][:, f], X.T @ duc),
+                              (dwd[e][f, :], dO.T @ (gc * s * uc))):
+                err = rel_err(got.cpu().numpy(), want)
+                assert err <= TOL_BF16, (e, int(f), err)
+    # input and gate gradients of tokens whose experts are all sampled
+    ok_tok = np.nonzero(np.all(np.isin(ids, S), axis=1))[0]
+    toks = rng.choice(ok_tok, size=min(24, len(ok_tok)), replace=False)
+    dx_h = dx.float().cpu().numpy()
+    dg_h = dg.cpu().numpy()
+    for t in toks:
+        want_dx = np.zeros(cfg.D)
+        for k in range(cfg.K):
+            e = int(ids[t, k])
+            wg, wu, wd = (w.astype(np.float64) for w in W[e])
+            dv, _, _, _ = oracle.backward.swiglu_ffn_backward(x[t][None], wg, wu, wd,
+                                                              gates[t, k] * dy[t][None])
+            want_dx += dv[0]
+            out = oracle.swiglu_ffn(x[t][None], wg, wu, wd)[0]
+            assert abs(dg_h[t, k] - dy[t] @ out) <= TOL_BF16 * np.abs(dy[t]).sum() * np.abs(
+                out).max(), (t, k)
+        assert rel_err(dx_h[t], want_dx) <= TOL_BF16, t
+    # the gradient return: every device's partials, summed, give the totals
+    acc = [torch.zeros_like(w) for w in (dwg, dwu, dwd)]
+    for d in range(cfg.P):
+        parts = L.backward(dy_dev, run.gates, run.gu, gut, dnt, d)[2:]
+        for a, p in zip(acc, parts):
+            a += p
+    torch.cuda.synchronize()
+    for a, tot in zip(acc, (dwg, dwu, dwd)):
+        den = tot.abs().max().item()
+        assert (a - tot).abs().max().item() <= 1e-5 * den
+    del acc
+    if name != "deepseek-v3":
+        L.set_mode("ep")
+        run.forward(-1)
+        dx_ep, dg_ep, dwg_ep = (t.clone() for t in L.backward(dy_dev, run.gates, run.gu, gut,
+                                                              dnt, -1)[:3])
+        torch.cuda.synchronize()
+        assert torch.equal(dx_ep, dx)
+        assert torch.equal(dg_ep, dg)
+        assert (dwg_ep - dwg).abs().max().item() <= 1e-5 * dwg.abs().max().item()
