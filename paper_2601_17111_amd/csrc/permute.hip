@@ -38,6 +38,31 @@ __global__ __launch_bounds__(256) void rank_kernel(
   const int nb = bits_for(uint32_t(E));
   const int64_t tile0 = int64_t(blockIdx.x) * kRankTile;
   const int64_t s0 = tile0 + int64_t(w) * kRankSub;
+  // Every global load is issued up front (the wave's ids and gates, kept in
+  // registers for both passes; the tile's base row; the chunk table), so
+  // the kernel waits on memory once instead of once per step.
+  static_assert(kRankWaves * kWave == 256, "one rank tile per 256-thread workgroup");
+  constexpr int kIter = kRankSub / kWave;
+  constexpr int kBaseIter = (LLEP_MAX_EXPERTS + 255) / 256;
+  uint32_t ev[kIter];
+  float gv[kIter];
+#pragma unroll
+  for (int j = 0; j < kIter; ++j) {
+    const int64_t p = s0 + j * kWave + lane_id();
+    int32_t v = E;  // sentinel: past the end or invalid
+    gv[j] = 0.0f;
+    if (p < R) {
+      v = ids[p];
+      gv[j] = gates[p];
+    }
+    ev[j] = v >= 0 && v < E ? uint32_t(v) : uint32_t(E);
+  }
+  int32_t rbv[kBaseIter];
+#pragma unroll
+  for (int i = 0; i < kBaseIter; ++i) {
+    const int e = tid + 256 * i;
+    rbv[i] = e < E ? rank_base[int64_t(blockIdx.x) * E + e] : 0;
+  }
   const int nc = min(max(expert_chunk_begin[E], 0), min(max_chunks, kMaxChunks));
   for (int i = tid; i < kRankWaves * E; i += blockDim.x) wbase[i] = 0;
   for (int i = tid; i <= E; i += blockDim.x) ecb[i] = min(max(expert_chunk_begin[i], 0), nc);
@@ -49,21 +74,19 @@ __global__ __launch_bounds__(256) void rank_kernel(
   __syncthreads();
 
   // pass A: per-wave counts of each expert in the wave's slice
-  for (int j = 0; j < kRankSub; j += kWave) {
-    if (s0 + j >= R) break;
-    const int64_t p = s0 + j + lane_id();
-    uint32_t e = uint32_t(E);
-    if (p < R) {
-      const int32_t v = ids[p];
-      if (v >= 0 && v < E) e = uint32_t(v);
-    }
+#pragma unroll
+  for (int j = 0; j < kIter; ++j) {
+    const uint32_t e = ev[j];
     const uint64_t m = match_any(e, nb);
     if (e < uint32_t(E) && (m & lanemask_lt()) == 0) wbase[w * E + e] += __popcll(m);
   }
   __syncthreads();
   // wave bases = tile base + counts of the earlier waves of the tile
-  for (int e = tid; e < E; e += blockDim.x) {
-    int32_t run = rank_base[int64_t(blockIdx.x) * E + e];
+#pragma unroll
+  for (int i = 0; i < kBaseIter; ++i) {
+    const int e = tid + 256 * i;
+    if (e >= E) continue;
+    int32_t run = rbv[i];
     for (int v = 0; v < kRankWaves; ++v) {
       const int32_t c = wbase[v * E + e];
       wbase[v * E + e] = run;
@@ -73,14 +96,10 @@ __global__ __launch_bounds__(256) void rank_kernel(
   __syncthreads();
 
   // pass B: rank, locate the chunk, write the row
-  for (int j = 0; j < kRankSub; j += kWave) {
-    if (s0 + j >= R) break;
-    const int64_t p = s0 + j + lane_id();
-    uint32_t e = uint32_t(E);
-    if (p < R) {
-      const int32_t v = ids[p];
-      if (v >= 0 && v < E) e = uint32_t(v);
-    }
+#pragma unroll
+  for (int j = 0; j < kIter; ++j) {
+    const int64_t p = s0 + j * kWave + lane_id();
+    const uint32_t e = ev[j];
     const uint64_t m = match_any(e, nb);
     int32_t r = 0;
     if (e < uint32_t(E)) r = wbase[w * E + e] + __popcll(m & lanemask_lt());
@@ -97,7 +116,7 @@ __global__ __launch_bounds__(256) void rank_kernel(
       pair_row[p] = row;
       if (row >= 0 && row < R) {
         row_pair[row] = int32_t(p);
-        gate_perm[row] = gates[p];
+        gate_perm[row] = gv[j];
       }
     } else if (p < R) {
       pair_row[p] = -1;
@@ -109,7 +128,9 @@ __global__ __launch_bounds__(256) void rank_kernel(
 // qwen3-30b layer shapes inside the full step: non-temporal loads of
 // out_perm raise the combine from 0.62-0.65 to 0.73-0.79 of HBM peak;
 // non-temporal loads in the gather gain nothing and non-temporal stores of
-// x_perm lose 10-15%. Four pairs' rows of at most 4 vectors per lane are in
+// x_perm lose 10-15%; a persistent gather that requests the next token's row
+// before storing the current one measured no faster (the gather moves its
+// bytes at 5.9 TB/s, four fifths of them writes; a plain fill reaches 6.8). Four pairs' rows of at most 4 vectors per lane are in
 // flight per combine step (1 or 2 measured within 2%).
 constexpr bool kGatherNtLoad = false;
 constexpr bool kGatherNtStore = false;
