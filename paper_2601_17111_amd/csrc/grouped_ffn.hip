@@ -33,7 +33,10 @@ constexpr int kTileM = 256;  // rows per GEMM tile (one m-tile never spans two g
 #ifndef LLEP_GEMM2_WAVES
 #define LLEP_GEMM2_WAVES LLEP_GEMM_WAVES
 #endif
-constexpr int kWavesM = 2, kWavesN = LLEP_GEMM_WAVES / 2;
+#ifndef LLEP_WAVES_M256
+#define LLEP_WAVES_M256 2
+#endif
+constexpr int kWavesM = LLEP_WAVES_M256, kWavesN = LLEP_GEMM_WAVES / LLEP_WAVES_M256;
 constexpr int kWavesM192 = LLEP_GEMM2_WAVES / 2, kWavesN192 = 2;
 #ifndef LLEP_GROUP_M
 #define LLEP_GROUP_M 8
@@ -149,9 +152,15 @@ struct GemmArgs {
   const int4 *tiles;        // forward: (group, m-tile, padded first row, 0)
   const int32_t *n_mtiles;
   int32_t N, Kdim;
-  // SwiGLU backward
-  const uint16_t *GU;  // blocked [padded rows][2F]: gate / up values
-  uint16_t *act;       // blocked [padded rows][F]
+  // SwiGLU backward: reads the recomputed gate / up values (blocked
+  // [padded rows][2F]); besides [d g | d u] in that layout (C) it writes
+  // [d g | d u] and the activation transposed into the weight-gradient
+  // layout: blocks of 16 columns x 32 rows over [columns][kmax], the rows of
+  // group g starting at kbase[g]
+  const uint16_t *GU;
+  uint16_t *dgu_t, *act_t;
+  const int32_t *kbase;
+  int64_t kmax;
   // multi-problem backward launch: weight-gradient tiles of the experts in
   // wg_experts (longest k-segment first), problem wp[0] then wp[1] per
   // expert, then the tiles of the main problem; tiles past the first gridDim
@@ -247,7 +256,7 @@ __device__ __forceinline__ int lds_swz32(int row, int kc) {
 }
 
 struct TileCoord {
-  int e, row0, prow0, m0, rows_valid, n0, cols_valid, k0, nk;
+  int e, row0, prow0, m0, rows_valid, n0, cols_valid, k0, nk, grp;
   int p, N;  // problem (0: the main one, 1 / 2: wp[0] / wp[1]) and its columns
 };
 
@@ -261,6 +270,7 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs &g, int u, int n_mt, 
   const int nt = rem / gm;
   const int4 te = g.tiles[sr * kGroupM + rem % gm];
   const int32_t *gr = g.groups + 4 * te.x;
+  t.grp = te.x;
   t.e = gr[1];
   t.row0 = gr[2];
   t.prow0 = te.z;
@@ -289,6 +299,7 @@ __device__ __forceinline__ void decode_tile_wg(const GemmArgs &g, int u, int per
   const int N = second ? g.wp[1].N : g.wp[0].N;
   const int n_nt = (N + BN - 1) / BN;
   const int4 we = g.wg_experts[i];
+  t.grp = 0;
   t.e = we.x;
   t.row0 = 0;
   t.prow0 = 0;
@@ -658,50 +669,80 @@ void gemm256_kernel(GemmArgs g) {
         }
       }
     } else if constexpr (kEpi == kEpiSwigluBwd) {
-      // C = d act [padded rows][F] for activation columns f. With g = gate,
-      // u = up (recomputed, blocked [padded rows][2F], gate f at column
-      // 64 (f / 32) + f % 32, up 32 further): d gate = d act u silu'(g),
-      // d up = d act silu(g), written in the same layout, and act = silu(g) u
-      // (blocked [padded rows][F]) for the down projection's weight gradient.
+      // C = d act for activation columns f. With g = gate, u = up
+      // (recomputed, blocked [padded rows][2F], gate f at column
+      // 64 (f / 32) + f % 32, up 32 further): d gate = d act u silu'(g) and
+      // d up = d act silu(g) go to C in the same layout (for dX), and d gate,
+      // d up and act = silu(g) u go transposed to the weight-gradient layout:
+      // a 32-row piece of the group is one 32-deep k-block there, staged in
+      // LDS as [column][row] (2 KB per 32 x 32 output) and stored as two
+      // 1 KB blocks. Rows past the group's end are written as zeros.
       static_assert(kCBlocked, "gate/up gradients are blocked over padded rows");
+      static_assert(3 * 2048 <= STAGING, "staging");
       const int F = int(g.ldc);
-      const int gu_blocks = (2 * F) >> 5, a_blocks = F >> 5;
+      const int gu_blocks = (2 * F) >> 5;
+      const int64_t kblocks = g.kmax >> 5;
+      const int kb_grp = g.kbase[c.grp];
+      uint16_t *st16 = reinterpret_cast<uint16_t *>(stg);
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         if (i * 32 >= rows_w) break;
-        const int pr = c.prow0 + c.m0 + wm * WM + i * 32 + (lane & 31);
+        const int rr = c.m0 + wm * WM + i * 32;  // first row of the piece in its group
+        const int pr = c.prow0 + rr + (lane & 31);
         const bool row_ok = i * 32 + (lane & 31) < rows_w;
+        const int64_t kb = (kb_grp + rr) >> 5;
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int col0 = c.n0 + wn * WN + j * 32;  // first activation column f
-          if (col0 >= g.N || !row_ok) continue;
+          if (col0 >= g.N) continue;
           const int64_t gblk = (int64_t(pr >> 4) * gu_blocks + (col0 >> 5) * 2) * 512 +
                                (pr & 15) * 32;
-          const int64_t ablk = (int64_t(pr >> 4) * a_blocks + (col0 >> 5)) * 512 + (pr & 15) * 32;
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
             const int cc = 8 * gq + 4 * h;  // column inside the 32-block
-            const uint2 gw = *reinterpret_cast<const uint2 *>(g.GU + gblk + cc);
-            const uint2 uw = *reinterpret_cast<const uint2 *>(g.GU + gblk + 512 + cc);
-            float dg[4], du[4], av[4];
+            float dg[4] = {0.f, 0.f, 0.f, 0.f}, du[4] = {0.f, 0.f, 0.f, 0.f},
+                  av[4] = {0.f, 0.f, 0.f, 0.f};
+            if (row_ok) {
+              const uint2 gw = *reinterpret_cast<const uint2 *>(g.GU + gblk + cc);
+              const uint2 uw = *reinterpret_cast<const uint2 *>(g.GU + gblk + 512 + cc);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t gbits = (e < 2 ? gw.x : gw.y) >> (16 * (e & 1));
+                const uint32_t ubits = (e < 2 ? uw.x : uw.y) >> (16 * (e & 1));
+                const float gv = __uint_as_float(gbits << 16), uv = __uint_as_float(ubits << 16);
+                const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-gv));
+                const float da = acc[i][j][4 * gq + e];
+                dg[e] = da * uv * (sg * (1.0f + gv * (1.0f - sg)));
+                du[e] = da * (gv * sg);
+                av[e] = gv * sg * uv;
+              }
+              uint16_t *dgu = g.C;
+              *reinterpret_cast<uint2 *>(dgu + gblk + cc) =
+                  make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
+              *reinterpret_cast<uint2 *>(dgu + gblk + 512 + cc) =
+                  make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));
+            }
+            // transposed staging: output o at o * 1024 elements, [column][row]
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const uint32_t gbits = (e < 2 ? gw.x : gw.y) >> (16 * (e & 1));
-              const uint32_t ubits = (e < 2 ? uw.x : uw.y) >> (16 * (e & 1));
-              const float gv = __uint_as_float(gbits << 16), uv = __uint_as_float(ubits << 16);
-              const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-gv));
-              const float da = acc[i][j][4 * gq + e];
-              dg[e] = da * uv * (sg * (1.0f + gv * (1.0f - sg)));
-              du[e] = da * (gv * sg);
-              av[e] = gv * sg * uv;
+              const int n = (cc + e) * 32 + (lane & 31);
+              st16[n] = f32_to_bf16(dg[e]);
+              st16[1024 + n] = f32_to_bf16(du[e]);
+              st16[2048 + n] = f32_to_bf16(av[e]);
             }
-            uint16_t *dgu = g.C;
-            *reinterpret_cast<uint2 *>(dgu + gblk + cc) =
-                make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
-            *reinterpret_cast<uint2 *>(dgu + gblk + 512 + cc) =
-                make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));
-            *reinterpret_cast<uint2 *>(g.act + ablk + cc) =
-                make_uint2(pack2(av[0], av[1]), pack2(av[2], av[3]));
+          }
+          // d gate rows 64 (f / 32) + 0..31 and d up rows + 32 of [2F][kmax];
+          // act rows f of [F][kmax]; 16 rows per 1 KB block
+          const int64_t ngate = 2 * col0;  // = 64 * (col0 / 32)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            const i32x4 vg = *reinterpret_cast<const i32x4 *>(stg + b * 1024 + lane * 16);
+            const i32x4 vu = *reinterpret_cast<const i32x4 *>(stg + 2048 + b * 1024 + lane * 16);
+            const i32x4 va = *reinterpret_cast<const i32x4 *>(stg + 4096 + b * 1024 + lane * 16);
+            *reinterpret_cast<i32x4 *>(g.dgu_t + (((ngate >> 4) + b) * kblocks + kb) * 512 + lane * 8) = vg;
+            *reinterpret_cast<i32x4 *>(g.dgu_t + ((((ngate + 32) >> 4) + b) * kblocks + kb) * 512 +
+                                       lane * 8) = vu;
+            *reinterpret_cast<i32x4 *>(g.act_t + (((col0 >> 4) + b) * kblocks + kb) * 512 + lane * 8) = va;
           }
         }
       }
@@ -1011,8 +1052,8 @@ hipError_t launch_pack(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const 
 // ---------------------------------------------------------------------------
 
 struct BwdLayout {
-  size_t tiles_off, wge_off, kbase_off, gprow_off, chunk_off;
-  size_t gu_off, dgu_off, act_off, xt_off, dot_off, actt_off, dgut_off, total;
+  size_t tiles_off, wge_off, kbase_off, chunk_off;
+  size_t gu_off, dgu_off, xt_off, dot_off, actt_off, dgut_off, total;
   int64_t max_groups, max_mtiles, prow_max, kmax;
 };
 
@@ -1028,11 +1069,9 @@ static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t 
   L.tiles_off = o;  o = round256(o + size_t(L.max_mtiles) * 16);
   L.wge_off = o;    o = round256(o + size_t(E) * 16);
   L.kbase_off = o;  o = round256(o + size_t(L.max_groups) * 4);
-  L.gprow_off = o;  o = round256(o + size_t(L.max_groups) * 4);
   L.chunk_off = o;  o = round256(o + size_t(L.kmax / 32) * 4);
   L.gu_off = o;     o = round256(o + size_t(L.prow_max) * 2 * F * 2);
   L.dgu_off = o;    o = round256(o + size_t(L.prow_max) * 2 * F * 2);
-  L.act_off = o;    o = round256(o + size_t(L.prow_max) * F * 2);
   L.xt_off = o;     o = round256(o + size_t(D) * L.kmax * 2);
   L.dot_off = o;    o = round256(o + size_t(D) * L.kmax * 2);
   L.actt_off = o;   o = round256(o + size_t(F) * L.kmax * 2);
@@ -1046,19 +1085,18 @@ size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, 
 }
 
 // One workgroup. For the groups [lo, hi) of the range: each group's first
-// weight-gradient row (kbase, a multiple of 32) in gradient-return order, its
-// first padded forward row (gprow, rows rounded to 16 per group, as the
-// tile list lays them out), the owner group of every 32-row chunk, and the
+// weight-gradient row (kbase[group], a multiple of 32) in gradient-return
+// order, the owner group of every 32-row chunk, and the
 // experts present with their segment (first 32-row slice, slices), longest
 // segment first (ties: lower expert id), so the work counter of the
 // multi-problem launch hands out the longest tiles first. Zeroes that
 // counter.
 __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
-    int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase, int32_t *__restrict__ gprow,
+    int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase,
     int32_t *__restrict__ chunk_group, int4 *__restrict__ wg_experts, int32_t *__restrict__ n_wg,
     int32_t *__restrict__ kslices, int32_t *__restrict__ queue) {
-  __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks], s16[kMaxChunks];
+  __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks];
   __shared__ int32_t esl[LLEP_MAX_EXPERTS];
   const int tid = threadIdx.x;
   const int lo = device < 0 ? group_begin[0] : group_begin[device];
@@ -1070,17 +1108,13 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     se[i] = e;
     skey[i] = d == e / M ? -1 : d;  // native device first
     ssl[i] = (n + 31) / 32;
-    s16[i] = (n + 15) / 16 * 16;
   }
   __syncthreads();
   for (int i = tid; i < G; i += blockDim.x) {
-    int32_t kb = 0, pr = 0;
-    for (int j = 0; j < G; ++j) {
+    int32_t kb = 0;
+    for (int j = 0; j < G; ++j)
       if (se[j] < se[i] || (se[j] == se[i] && skey[j] < skey[i])) kb += ssl[j];
-      if (j < i) pr += s16[j];
-    }
-    kbase[i] = kb * 32;
-    gprow[i] = pr;
+    kbase[lo + i] = kb * 32;
     for (int c = kb; c < kb + ssl[i]; ++c) chunk_group[c] = lo + i;
   }
   for (int e = tid; e < E; e += blockDim.x) {
@@ -1107,39 +1141,28 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
   }
 }
 
-// Copy C columns of the range's rows into the weight-gradient layout:
-// blocks of 16 columns x 32 rows over [C][kmax], row kbase[g] + r of the
-// layout = row r of group g (zero for the padding r >= n_g). The source is
-// row-major by x_perm row (ld elements) or blocked over padded rows.
-template <bool kBlocked>
+// Copy C columns of the range's rows (row-major by x_perm row, ld elements)
+// into the weight-gradient layout: blocks of 16 columns x 32 rows over
+// [C][kmax], row kbase[g] + r of the layout = row r of group g (zero for the
+// padding r >= n_g).
 __global__ __launch_bounds__(256) void to_wgrad_kernel(
     const uint16_t *__restrict__ src, int64_t ld, int32_t C, const int32_t *__restrict__ groups,
-    int32_t lo_dev, const int32_t *__restrict__ group_begin, int32_t P,
-    const int32_t *__restrict__ kbase, const int32_t *__restrict__ gprow,
-    const int32_t *__restrict__ chunk_group, const int32_t *__restrict__ kslices, int64_t kmax,
-    uint16_t *__restrict__ dst) {
+    const int32_t *__restrict__ kbase, const int32_t *__restrict__ chunk_group,
+    const int32_t *__restrict__ kslices, int64_t kmax, uint16_t *__restrict__ dst) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][40];
   const int t = threadIdx.x;
-  const int lo = lo_dev < 0 ? group_begin[0] : group_begin[lo_dev];
   const int64_t items = int64_t(*kslices) * (C / 64);
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int c = int(item / (C / 64)), cc = int(item % (C / 64));
-    const int gi = chunk_group[c], i = gi - lo;
+    const int gi = chunk_group[c];
     const int n = groups[4 * gi + 3];
-    const int r0 = c * 32 - kbase[i];
+    const int r0 = c * 32 - kbase[gi];
     {
       const int r = t >> 3, col = cc * 64 + (t & 7) * 8;
       i32x4 v = {0, 0, 0, 0};
       const int row = r0 + r;
-      if (row < n) {
-        if (kBlocked) {
-          const int pr = gprow[i] + row;
-          v = *reinterpret_cast<const i32x4 *>(
-              src + (int64_t(pr >> 4) * (C >> 5) + (col >> 5)) * 512 + (pr & 15) * 32 + (col & 31));
-        } else {
-          v = *reinterpret_cast<const i32x4 *>(src + int64_t(groups[4 * gi + 2] + row) * ld + col);
-        }
-      }
+      if (row < n)
+        v = *reinterpret_cast<const i32x4 *>(src + int64_t(groups[4 * gi + 2] + row) * ld + col);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         tile[(t & 7) * 8 + 2 * q][r] = uint16_t(uint32_t(v[q]) & 0xffffu);
@@ -1201,11 +1224,9 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   int4 *tiles = reinterpret_cast<int4 *>(ws + L.tiles_off);
   int4 *wge = reinterpret_cast<int4 *>(ws + L.wge_off);
   int32_t *kbase = reinterpret_cast<int32_t *>(ws + L.kbase_off);
-  int32_t *gprow = reinterpret_cast<int32_t *>(ws + L.gprow_off);
   int32_t *chunk = reinterpret_cast<int32_t *>(ws + L.chunk_off);
   uint16_t *gu = reinterpret_cast<uint16_t *>(ws + L.gu_off);
   uint16_t *dgu = reinterpret_cast<uint16_t *>(ws + L.dgu_off);
-  uint16_t *act = reinterpret_cast<uint16_t *>(ws + L.act_off);
   uint16_t *xt = reinterpret_cast<uint16_t *>(ws + L.xt_off);
   uint16_t *dot = reinterpret_cast<uint16_t *>(ws + L.dot_off);
   uint16_t *actt = reinterpret_cast<uint16_t *>(ws + L.actt_off);
@@ -1222,8 +1243,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
                      a.device, a.P, kTileM, tiles, n_mtiles);
   LLEP_CHECK_LAUNCH();
   hipLaunchKernelGGL(wgrad_table_kernel, dim3(1), dim3(1024), 0, stream, a.groups, a.group_begin,
-                     a.device, a.P, a.E, a.E / a.P, kbase, gprow, chunk, wge, n_wg, kslices,
-                     queue);
+                     a.device, a.P, a.E, a.E / a.P, kbase, chunk, wge, n_wg, kslices, queue);
   LLEP_CHECK_LAUNCH();
   constexpr int NT = 64 * kWavesM * kWavesN;
   constexpr int NT192 = 64 * kWavesM192 * kWavesN192;
@@ -1246,7 +1266,8 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, false, true>), dim3(grid),
                      dim3(NT), 0, stream, g);
   LLEP_CHECK_LAUNCH();
-  // 2. d act = d out Wd^T; epilogue writes d g, d u (into dgu) and act
+  // 2. d act = d out Wd^T; the epilogue writes [d g | d u] blocked (for dX)
+  // and [d g | d u], act transposed into the weight-gradient layout
   GemmArgs g2 = g;
   g2.A = static_cast<const uint16_t *>(a.d_out_perm);
   g2.lda = D;
@@ -1258,7 +1279,10 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   g2.N = F;
   g2.Kdim = D;
   g2.GU = gu;
-  g2.act = act;
+  g2.dgu_t = dgut;
+  g2.act_t = actt;
+  g2.kbase = kbase;
+  g2.kmax = L.kmax;
   if (f192)
     hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiSwigluBwd, false, true>),
                        dim3(grid), dim3(NT192), 0, stream, g2);
@@ -1266,24 +1290,16 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
     hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiSwigluBwd, false, true>),
                        dim3(grid), dim3(NT), 0, stream, g2);
   LLEP_CHECK_LAUNCH();
-  // 3. the weight-gradient operands: X, d out, act and [d g | d u] with the
-  // rows of each expert laid end to end along k (gradient-return order)
+  // 3. the other weight-gradient operands, X and d out, with the rows of
+  // each expert laid end to end along k (gradient-return order)
   const int tg = 4 * grid;
-  hipLaunchKernelGGL(to_wgrad_kernel<false>, dim3(tg), dim3(256), 0, stream,
-                     static_cast<const uint16_t *>(a.x_perm), int64_t(D), D, a.groups, a.device,
-                     a.group_begin, a.P, kbase, gprow, chunk, kslices, L.kmax, xt);
+  hipLaunchKernelGGL(to_wgrad_kernel, dim3(tg), dim3(256), 0, stream,
+                     static_cast<const uint16_t *>(a.x_perm), int64_t(D), D, a.groups, kbase,
+                     chunk, kslices, L.kmax, xt);
   LLEP_CHECK_LAUNCH();
-  hipLaunchKernelGGL(to_wgrad_kernel<false>, dim3(tg), dim3(256), 0, stream,
-                     static_cast<const uint16_t *>(a.d_out_perm), int64_t(D), D, a.groups,
-                     a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices, L.kmax, dot);
-  LLEP_CHECK_LAUNCH();
-  hipLaunchKernelGGL(to_wgrad_kernel<true>, dim3(tg), dim3(256), 0, stream, act, int64_t(F), F,
-                     a.groups, a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices, L.kmax,
-                     actt);
-  LLEP_CHECK_LAUNCH();
-  hipLaunchKernelGGL(to_wgrad_kernel<true>, dim3(tg), dim3(256), 0, stream, dgu, int64_t(2 * F),
-                     2 * F, a.groups, a.device, a.group_begin, a.P, kbase, gprow, chunk, kslices,
-                     L.kmax, dgut);
+  hipLaunchKernelGGL(to_wgrad_kernel, dim3(tg), dim3(256), 0, stream,
+                     static_cast<const uint16_t *>(a.d_out_perm), int64_t(D), D, a.groups, kbase,
+                     chunk, kslices, L.kmax, dot);
   LLEP_CHECK_LAUNCH();
   // 4. one launch: dX = [d g | d u] [Wg | Wu]^T into the x_perm rows, and
   // the weight gradients X^T [d g | d u] (de-interleaved into dWg, dWu) and
