@@ -95,7 +95,8 @@ def test_combine_backward_rows_and_gates(dev):
     assert np.allclose(got_g, want_g, rtol=1e-5, atol=1e-5 * np.abs(want_g).max())
 
 
-@pytest.mark.parametrize("T,K,D", [(37, 70, 4096), (200, 5, 136), (3, 4, 8)])
+@pytest.mark.parametrize("T,K,D", [(37, 70, 4096), (200, 5, 136), (3, 4, 8), (50, 4, 2560),
+                                   (41, 6, 2880)])
 def test_combine_backward_standalone(dev, T, K, D):
     """Rows longer than one wave slice, rows of a ragged number of vectors,
     K > 64 (two 64-pair batches), and an invalid pair."""
