@@ -533,49 +533,82 @@ void gemm256_kernel(GemmArgs g) {
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
-    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-    // slice kt sits in stage kt % kStages; st tracks the slice being read,
-    // st_req the stage of slice kt + kAhead
-    int st = 0, st_req = kAhead % kStages, kt_req = kAhead;
-    // slices 0 .. min(kAhead, nk) - 1 were requested; wait for slice 0
-    if (nk >= kAhead)
-      wait_and_sync<(kAhead - 1) * PER_STAGE>();
-    else
-      wait_and_sync<0>();
-    read_frags(st, 0, fa0, fb0);
-    int kt = 0;
-    // steady state: request slice kt + kAhead, three slices stay in flight
-    // past slice kt + 1 (compile-time wait count). The last slice is peeled
-    // so no branch joins around the LDS reads (the wait inserted at such a
-    // join would drain the fresh reads).
-    for (; kt < nk - kAhead; ++kt) {
-      // k-step 0 of slice kt; reads of its k-step 1; DMA of slice kt + kAhead
-      interleaved_step(acc, fa0, fb0, fa1, fb1, st, 1, true, st_req, kt_req);
-      st_req = next_stage(st_req);
-      ++kt_req;
-      wait_and_sync<(kAhead - 1) * PER_STAGE>();
-      st = next_stage(st);
-      // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1
-      interleaved_step(acc, fa1, fb1, fa0, fb0, st, 0, false, 0, 0);
-    }
-    // tail: everything is requested; nk - 2 - kt slices remain past kt + 1
-    for (; kt < nk - 1; ++kt) {
-      read_frags(st, 1, fa1, fb1);
-      mfma_step(acc, fa0, fb0);
-      const int left = nk - 2 - kt;
-      if (left >= 2)
-        wait_and_sync<2 * PER_STAGE>();
-      else if (left == 1)
-        wait_and_sync<PER_STAGE>();
+    // A wave whose 32 x 32 blocks all lie past the tile's last valid row or
+    // column (a group's last, partly filled m-tile; the last n-tile) has no
+    // MFMA work: it runs the same slice loop with the same DMA requests and
+    // barriers, without LDS reads or MFMAs (its accumulators stay zero and
+    // the epilogue stores none of its rows or columns).
+    // (wave-uniform in a scalar register, so both sides hold their barriers
+    // as a uniform branch)
+    const int active =
+        __builtin_amdgcn_readfirstlane(int(t.rows_valid > wm * WM && t.cols_valid > wn * WN));
+    if (active) {
+      bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+      // slice kt sits in stage kt % kStages; st tracks the slice being read,
+      // st_req the stage of slice kt + kAhead
+      int st = 0, st_req = kAhead % kStages, kt_req = kAhead;
+      // slices 0 .. min(kAhead, nk) - 1 were requested; wait for slice 0
+      if (nk >= kAhead)
+        wait_and_sync<(kAhead - 1) * PER_STAGE>();
       else
         wait_and_sync<0>();
-      st = next_stage(st);
       read_frags(st, 0, fa0, fb0);
+      int kt = 0;
+      // steady state: request slice kt + kAhead, three slices stay in flight
+      // past slice kt + 1 (compile-time wait count). The last slice is peeled
+      // so no branch joins around the LDS reads (the wait inserted at such a
+      // join would drain the fresh reads).
+      for (; kt < nk - kAhead; ++kt) {
+        // k-step 0 of slice kt; reads of its k-step 1; DMA of slice kt + kAhead
+        interleaved_step(acc, fa0, fb0, fa1, fb1, st, 1, true, st_req, kt_req);
+        st_req = next_stage(st_req);
+        ++kt_req;
+        wait_and_sync<(kAhead - 1) * PER_STAGE>();
+        st = next_stage(st);
+        // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1
+        interleaved_step(acc, fa1, fb1, fa0, fb0, st, 0, false, 0, 0);
+      }
+      // tail: everything is requested; nk - 2 - kt slices remain past kt + 1
+      for (; kt < nk - 1; ++kt) {
+        read_frags(st, 1, fa1, fb1);
+        mfma_step(acc, fa0, fb0);
+        const int left = nk - 2 - kt;
+        if (left >= 2)
+          wait_and_sync<2 * PER_STAGE>();
+        else if (left == 1)
+          wait_and_sync<PER_STAGE>();
+        else
+          wait_and_sync<0>();
+        st = next_stage(st);
+        read_frags(st, 0, fa0, fb0);
+        mfma_step(acc, fa1, fb1);
+      }
+      read_frags(st, 1, fa1, fb1);
+      mfma_step(acc, fa0, fb0);
       mfma_step(acc, fa1, fb1);
+    } else {
+      int st_req = kAhead % kStages, kt_req = kAhead;
+      if (nk >= kAhead)
+        wait_and_sync<(kAhead - 1) * PER_STAGE>();
+      else
+        wait_and_sync<0>();
+      int kt = 0;
+      for (; kt < nk - kAhead; ++kt) {
+        issue(st_req, kt_req);
+        st_req = next_stage(st_req);
+        ++kt_req;
+        wait_and_sync<(kAhead - 1) * PER_STAGE>();
+      }
+      for (; kt < nk - 1; ++kt) {
+        const int left = nk - 2 - kt;
+        if (left >= 2)
+          wait_and_sync<2 * PER_STAGE>();
+        else if (left == 1)
+          wait_and_sync<PER_STAGE>();
+        else
+          wait_and_sync<0>();
+      }
     }
-    read_frags(st, 1, fa1, fb1);
-    mfma_step(acc, fa0, fb0);
-    mfma_step(acc, fa1, fb1);
     // every wave is done with the ring before the next tile's slices land
     __syncthreads();
     const TileCoord c = t;
