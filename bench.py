@@ -46,6 +46,8 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ep", action="store_true", help="skip the standard-EP comparison")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
+    ap.add_argument("--no-full-layer", action="store_true",
+                    help="skip the all-devices grouped FFN measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before warmup, run a plain 1 GiB -> 1 GiB elementwise copy (torch.neg on "
                          "float32) three times: a kernel of known traffic that scales the HBM "
@@ -463,13 +465,14 @@ def main():
     out["m_local_GB"] = {"llep_max": max(m_llep), "llep_per_device": m_llep}
 
     # the raw 1-GPU layer: all P devices' groups back to back in one call
-    ms_full, seg_full = _time_steps(layer, run, max(3, args.steps // 4), -1)
-    total_rows = sum(dev_rows)
-    out["full_layer_all_devices"] = {
-        "ms_per_step": ms_full, "tokens_per_s": T / (ms_full * 1e-3), "segments_ms": seg_full,
-        "rows": total_rows,
-        "grouped_ffn_TFLOPs": 6.0 * D * F * total_rows / (seg_full["grouped_ffn"] * 1e-3) / 1e12,
-    }
+    if not args.no_full_layer:
+        ms_full, seg_full = _time_steps(layer, run, max(3, args.steps // 4), -1)
+        total_rows = sum(dev_rows)
+        out["full_layer_all_devices"] = {
+            "ms_per_step": ms_full, "tokens_per_s": T / (ms_full * 1e-3), "segments_ms": seg_full,
+            "rows": total_rows,
+            "grouped_ffn_TFLOPs": 6.0 * D * F * total_rows / (seg_full["grouped_ffn"] * 1e-3) / 1e12,
+        }
 
     if cfg.dtype == "bf16" and not args.no_backward:
         out["backward"] = _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows,

@@ -280,3 +280,38 @@ def test_backward_rejects_bad_arguments(dev):
     with pytest.raises(B.LLEPError) as ei:
         B.llep_pack_weights_backward(z, z, z)
     assert ei.value.code == B.LLEP_E_DTYPE
+
+
+def test_backward_force_assign_plan(dev):
+    """A plan where Alg. 3 force-assigns (min chunk 150 under capacity
+    ceil(R / P)): per-device partials against the oracle's partials of the
+    same plan, and the totals against the plan-free gradients."""
+    cfg = _cfg("bwd-force", alpha=(1, 1), routing=("hot", 0.5, 3), T=700, D=128, F=192, E=8,
+               K=3, P=4).with_(min_chunk=150)
+    run = BwdRun(cfg, 9, dev)
+    tot = [t.copy() for t in run.backward(-1)]
+    ids_flat = run.inp.ids.reshape(-1)
+    pl = oracle.plan(ids_flat.tolist(), cfg.E, cfg.P, cfg.capacity, cfg.min_chunk, lam=cfg.lam)
+    assert pl.forced > 0
+    assert run.layer.bufs.info_dict()["forced"] == pl.forced
+    assert run.layer.bufs.groups[:len(pl.groups)].cpu().tolist() == [list(g) for g in pl.groups]
+    _, row_pair = oracle.permute(ids_flat.tolist(), pl, cfg.E)
+    W = run.host_weights(range(cfg.E))
+    x = run.x.float().cpu().numpy()
+    dy = run.dy.float().cpu().numpy()
+    _, partials, dW = oracle.plan_backward(x, ids_flat, run.inp.gates.reshape(-1), lambda e: W[e],
+                                           dy, pl, np.asarray(row_pair), cfg.K, cfg.E // cfg.P)
+    want_dx, want_dg, _ = oracle.moe_backward(x, run.inp.ids, run.inp.gates, lambda e: W[e], dy,
+                                              cfg.E)
+    assert rel_err(tot[0], want_dx) <= TOL_BF16
+    assert rel_err(tot[1], want_dg) <= TOL_BF16
+    for e, want in dW.items():
+        for got, w in zip((tot[2][e], tot[3][e], tot[4][e]), want):
+            assert rel_err(got, w) <= TOL_BF16, e
+    for d in range(cfg.P):
+        parts = run.backward(d)[2:]
+        for (dd, e), want in partials.items():
+            if dd != d:
+                continue
+            for got, w in zip((p[e] for p in parts), want):
+                assert rel_err(got, w) <= TOL_BF16, (d, e)
