@@ -22,6 +22,11 @@
  *   llep_combine      gate-weighted sum of each token's K expert rows (Eq. 1;
  *                     Alg. 4 reverse_sort, reshape, sum over K)
  *
+ * and the backward of steps 4 and 5 (LLEP stays exact under training; the
+ * weight gradients of spilled chunks return to the expert's native device,
+ * Sec. 1 and Sec. 4): llep_combine_backward, llep_grouped_ffn_backward, and
+ * llep_combine with null gates to sum the pairs' input gradients per token.
+ *
  * Conventions for every entry point:
  *   - Every array argument is a DEVICE pointer, allocated and owned by the
  *     caller; the library never allocates, frees or keeps a pointer after the

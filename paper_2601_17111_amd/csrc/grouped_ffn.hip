@@ -11,9 +11,11 @@
 // groups. Tiles are handed out so that the workgroups resident on one XCD
 // (the hardware deals workgroup ids round-robin over the 8 XCDs) work on
 // neighbouring tiles, which share operand panels in that XCD's L2. Each tile
-// is 256 x BN, four waves of 128 x BN/2, v_mfma_f32_32x32x16_bf16 with fp32
-// accumulators in AGPRs; operands stream global -> LDS by DMA through a ring
-// of 32-deep k-slices, and MFMA fragments are double-buffered in registers.
+// is 256 x BN, eight waves (two per SIMD) with v_mfma_f32_32x32x16_bf16 and
+// fp32 accumulators in registers; operands stream global -> LDS by DMA
+// through a ring of 32-deep k-slices, and MFMA fragments are double-buffered
+// in registers. The same kernel serves the backward's GEMMs (see the
+// epilogues below).
 //
 // Packed weights (llep_pack_weights) keep the contraction dimension last, so
 // both GEMMs read 16-byte runs along K for A and B alike. In the gate/up
@@ -33,6 +35,8 @@ constexpr int kTileM = 256;  // rows per GEMM tile (one m-tile never spans two g
 #ifndef LLEP_GEMM2_WAVES
 #define LLEP_GEMM2_WAVES LLEP_GEMM_WAVES
 #endif
+// waves along M of the 256 x 256 tile: 2 x 4 (128 x 64 per wave); 4 x 2
+// (64 x 128) measured within 1% of it
 #ifndef LLEP_WAVES_M256
 #define LLEP_WAVES_M256 2
 #endif
@@ -173,13 +177,13 @@ struct GemmArgs {
 
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA grouped GEMM, 256 x BN tiles, 4 waves of 128 x BN/2.
+// bf16 MFMA grouped GEMM, 256 x BN tiles, eight waves of WM x WN.
 //
 // Operand tiles move global -> LDS directly (global_load_lds_dwordx4: no VGPR
-// staging) in k-slices of 32, through a ring of 4 LDS stages with 3 slices
-// in flight, so each slice has three k-steps of MFMA work (~3000 cycles) to
-// arrive. Waits count outstanding DMA instructions (they complete in issue
-// order), one barrier per k-step.
+// staging) in k-slices of 32, through a ring of kStages LDS stages with
+// kAhead slices requested ahead of the one being read. Waits count
+// outstanding DMA instructions (they complete in issue order), one barrier
+// per slice.
 //
 // LDS stage layout: rows of 32 bf16 (64 B = 4 chunks of 16 B); chunk index
 // XORed with (row / 4) % 4. A ds_read_b128 serves 16 lanes per cycle from 64
@@ -717,27 +721,47 @@ void gemm256_kernel(GemmArgs g) {
       const int64_t kblocks = g.kmax >> 5;
       const int kb_grp = g.kbase[c.grp];
       uint16_t *st16 = reinterpret_cast<uint16_t *>(stg);
+      // The 32 x 32 blocks go in order b = i TN + j; block b + 1's gate / up
+      // values are requested before block b is computed and stored, so their
+      // latency hides behind that work (the loads would otherwise wait for
+      // the stores before them, which the compiler cannot reorder).
+      auto block_ok = [&](int i, int j) {
+        return i * 32 < rows_w && c.n0 + wn * WN + j * 32 < g.N;
+      };
+      auto gu_index = [&](int i, int j) {
+        const int pr = c.prow0 + c.m0 + wm * WM + i * 32 + (lane & 31);
+        const int col0 = c.n0 + wn * WN + j * 32;
+        return (int64_t(pr >> 4) * gu_blocks + (col0 >> 5) * 2) * 512 + (pr & 15) * 32;
+      };
+      auto load_block = [&](int i, int j, uint2 (&gw)[4], uint2 (&uw)[4]) {
+        const bool ok = block_ok(i, j) && i * 32 + (lane & 31) < rows_w;
+        const int64_t gb = ok ? gu_index(i, j) : 0;
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        if (i * 32 >= rows_w) break;
-        const int rr = c.m0 + wm * WM + i * 32;  // first row of the piece in its group
-        const int pr = c.prow0 + rr + (lane & 31);
-        const bool row_ok = i * 32 + (lane & 31) < rows_w;
-        const int64_t kb = (kb_grp + rr) >> 5;
+        for (int gq = 0; gq < 4; ++gq) {
+          const int cc = 8 * gq + 4 * h;
+          gw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + cc) : make_uint2(0u, 0u);
+          uw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + 512 + cc) : make_uint2(0u, 0u);
+        }
+      };
+      uint2 gcur[4], ucur[4], gnxt[4], unxt[4];
+      load_block(0, 0, gcur, ucur);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
+      for (int b = 0; b < TM * TN; ++b) {
+        const int i = b / TN, j = b % TN;
+        if (b + 1 < TM * TN) load_block((b + 1) / TN, (b + 1) % TN, gnxt, unxt);
+        if (block_ok(i, j)) {
+          const int rr = c.m0 + wm * WM + i * 32;  // first row of the piece in its group
+          const bool row_ok = i * 32 + (lane & 31) < rows_w;
+          const int64_t kb = (kb_grp + rr) >> 5;
           const int col0 = c.n0 + wn * WN + j * 32;  // first activation column f
-          if (col0 >= g.N) continue;
-          const int64_t gblk = (int64_t(pr >> 4) * gu_blocks + (col0 >> 5) * 2) * 512 +
-                               (pr & 15) * 32;
+          const int64_t gblk = gu_index(i, j);
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
             const int cc = 8 * gq + 4 * h;  // column inside the 32-block
             float dg[4] = {0.f, 0.f, 0.f, 0.f}, du[4] = {0.f, 0.f, 0.f, 0.f},
                   av[4] = {0.f, 0.f, 0.f, 0.f};
             if (row_ok) {
-              const uint2 gw = *reinterpret_cast<const uint2 *>(g.GU + gblk + cc);
-              const uint2 uw = *reinterpret_cast<const uint2 *>(g.GU + gblk + 512 + cc);
+              const uint2 gw = gcur[gq], uw = ucur[gq];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 const uint32_t gbits = (e < 2 ? gw.x : gw.y) >> (16 * (e & 1));
@@ -768,14 +792,23 @@ void gemm256_kernel(GemmArgs g) {
           // act rows f of [F][kmax]; 16 rows per 1 KB block
           const int64_t ngate = 2 * col0;  // = 64 * (col0 / 32)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) {
-            const i32x4 vg = *reinterpret_cast<const i32x4 *>(stg + b * 1024 + lane * 16);
-            const i32x4 vu = *reinterpret_cast<const i32x4 *>(stg + 2048 + b * 1024 + lane * 16);
-            const i32x4 va = *reinterpret_cast<const i32x4 *>(stg + 4096 + b * 1024 + lane * 16);
-            *reinterpret_cast<i32x4 *>(g.dgu_t + (((ngate >> 4) + b) * kblocks + kb) * 512 + lane * 8) = vg;
-            *reinterpret_cast<i32x4 *>(g.dgu_t + ((((ngate + 32) >> 4) + b) * kblocks + kb) * 512 +
+          for (int bb = 0; bb < 2; ++bb) {
+            const i32x4 vg = *reinterpret_cast<const i32x4 *>(stg + bb * 1024 + lane * 16);
+            const i32x4 vu = *reinterpret_cast<const i32x4 *>(stg + 2048 + bb * 1024 + lane * 16);
+            const i32x4 va = *reinterpret_cast<const i32x4 *>(stg + 4096 + bb * 1024 + lane * 16);
+            *reinterpret_cast<i32x4 *>(g.dgu_t + (((ngate >> 4) + bb) * kblocks + kb) * 512 +
+                                       lane * 8) = vg;
+            *reinterpret_cast<i32x4 *>(g.dgu_t + ((((ngate + 32) >> 4) + bb) * kblocks + kb) * 512 +
                                        lane * 8) = vu;
-            *reinterpret_cast<i32x4 *>(g.act_t + (((col0 >> 4) + b) * kblocks + kb) * 512 + lane * 8) = va;
+            *reinterpret_cast<i32x4 *>(g.act_t + (((col0 >> 4) + bb) * kblocks + kb) * 512 +
+                                       lane * 8) = va;
+          }
+        }
+        if (b + 1 < TM * TN) {
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+            gcur[gq] = gnxt[gq];
+            ucur[gq] = unxt[gq];
           }
         }
       }
