@@ -315,3 +315,27 @@ def test_backward_force_assign_plan(dev):
                 continue
             for got, w in zip((p[e] for p in parts), want):
                 assert rel_err(got, w) <= TOL_BF16, (d, e)
+
+
+def test_backward_with_invalid_ids(dev):
+    """Pairs routed to an id outside [0, E) contribute nothing to any
+    gradient and get a zero gate gradient, as in the plan-free definition."""
+    import torch
+    cfg = _cfg("bwd-bad", T=300, D=128, F=128, E=8, K=2, P=4, routing=("hot", 0.5, 1))
+    run = BwdRun(cfg, 0, dev)
+    ids = run.inp.ids.copy()
+    ids[[3, 50, 299], [0, 1, 0]] = [8, -5, 100]
+    run.inp.ids = ids
+    run.ids = torch.from_numpy(ids).to(dev)
+    dx, dgates, dwg, dwu, dwd = run.backward(-1)
+    assert run.layer.bufs.info_dict()["status"] & 1
+    W = run.host_weights(range(cfg.E))
+    want_dx, want_dg, want_dW = oracle.moe_backward(run.x.float().cpu().numpy(), ids, run.inp.gates,
+                                                    lambda e: W[e], run.dy.float().cpu().numpy(),
+                                                    cfg.E)
+    assert rel_err(dx, want_dx) <= TOL_BF16
+    assert rel_err(dgates, want_dg) <= TOL_BF16
+    assert dgates[3, 0] == 0.0 and dgates[50, 1] == 0.0 and dgates[299, 0] == 0.0
+    for e, want in want_dW.items():
+        for got, w in zip((dwg[e], dwu[e], dwd[e]), want):
+            assert rel_err(got, w) <= TOL_BF16, e
