@@ -226,11 +226,11 @@ int llep_combine(const llep_plan_params *params, const void *out_perm,
  */
 
 /* Backward of Eq. (1). For every pair p = t*K + k with r = pair_row[p] >= 0:
- *   d_out_perm[r] = topk_gates[p] * dy[t]        (rounded once to bf16)
+ *   d_out_perm[r] = topk_gates[p] * dy[t]        (rounded once to dtype)
  *   d_gates[p]    = sum_i dy[t][i] * out_perm[r][i]   (float32)
  * and d_gates[p] = 0 when pair_row[p] < 0. out_perm [T*K][D] (the forward's
- * expert outputs), dy [T][D], d_out_perm [T*K][D], d_gates [T*K] float32.
- * Requires dtype == LLEP_BF16.
+ * expert outputs), dy [T][D], d_out_perm [T*K][D] in dtype; d_gates [T*K]
+ * float32.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
 int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
                           const int32_t *pair_row, const float *topk_gates,
@@ -245,7 +245,7 @@ int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
  *                                 w_up[d][32j + c] (the forward's gate/up
  *                                 interleave along the contraction);
  *   w_down_t_packed    [E][F*D]:  K = D; P row f = row f of w_down.
- * Requires dtype == LLEP_BF16, D % 64 == 0, F % 64 == 0.
+ * Requires D % 64 == 0, F % 64 == 0.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
 int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype,
                                const void *w_gate, const void *w_up,
@@ -255,9 +255,9 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
 /* Backward of step 4 for the groups of `device` (or of all devices when
  * device == -1). With X = x_perm[rows of a group (d, e, s, n)] and
  * dO = d_out_perm[same rows] (from llep_combine_backward):
- *   g = X Wg_e, u = X Wu_e (recomputed, rounded to bf16), dA = dO Wd_e^T,
+ *   g = X Wg_e, u = X Wu_e (recomputed), dA = dO Wd_e^T,
  *   dg = dA * u * silu'(g), du = dA * silu(g), act = silu(g) * u
- *   dx_perm[rows] = dg Wg_e^T + du Wu_e^T               (bf16)
+ *   dx_perm[rows] = dg Wg_e^T + du Wu_e^T               (dtype)
  * and, per expert e with groups in the range, the weight gradients in
  * float32 (dw_gate, dw_up [E][D][F], dw_down [E][F][D]):
  *   dWg_e = sum over e's groups of X^T dg, dWu_e of X^T du, dWd_e of act^T dO
@@ -267,9 +267,11 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
  * totals each native device holds after the gradient return. Experts without
  * a group in the range are not written; rows outside the range are not
  * written. Weights are the llep_pack_weights (w_gate_up_packed) and
- * llep_pack_weights_backward outputs. Workspace of at least
+ * llep_pack_weights_backward outputs. bf16 uses matrix cores and rounds g,
+ * u, dg, du and act to bf16 once each; f32 is a plain reference-precision
+ * path (no intermediate rounding). Workspace of at least
  * llep_grouped_ffn_backward_workspace_bytes bytes, 256-byte aligned.
- * Requires dtype == LLEP_BF16, D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned.
+ * Requires D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */
 size_t llep_grouped_ffn_backward_workspace_bytes(const llep_plan_params *params,
                                                  int32_t D, int32_t F,

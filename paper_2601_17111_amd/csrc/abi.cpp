@@ -240,7 +240,6 @@ int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
   int rc = check_params(params);
   if (rc != LLEP_OK) return rc;
   if ((rc = check_rows(D, dtype)) != LLEP_OK) return rc;
-  if (dtype != LLEP_BF16) return fail(LLEP_E_DTYPE, "the backward supports bf16 only");
   if (params->T > 0 && (!out_perm || !pair_row || !topk_gates || !dy || !d_out_perm || !d_gates))
     return fail(LLEP_E_ARG, "a data pointer is null");
   if (!aligned16(out_perm) || !aligned16(dy) || !aligned16(d_out_perm))
@@ -249,6 +248,7 @@ int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
   a.T = params->T;
   a.K = params->K;
   a.D = D;
+  a.dtype = dtype;
   a.out_perm = out_perm;
   a.dy = dy;
   a.pair_row = pair_row;
@@ -265,20 +265,20 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
   if (E < 1 || E > LLEP_MAX_EXPERTS) return fail(LLEP_E_ARG, "E outside [1, LLEP_MAX_EXPERTS]");
   int rc = check_ffn_dims(D, F, dtype);
   if (rc != LLEP_OK) return rc;
-  if (dtype != LLEP_BF16) return fail(LLEP_E_DTYPE, "the backward supports bf16 only");
   if (!w_gate || !w_up || !w_down || !w_gate_up_t_packed || !w_down_t_packed)
     return fail(LLEP_E_ARG, "a weight pointer is null");
   if (!aligned16(w_gate_up_t_packed) || !aligned16(w_down_t_packed))
     return fail(LLEP_E_ARG, "packed weights not 16-byte aligned");
-  return hip_result(llep::launch_pack_backward(E, D, F, w_gate, w_up, w_down, w_gate_up_t_packed,
-                                               w_down_t_packed, stream),
+  return hip_result(llep::launch_pack_backward(E, D, F, dtype, w_gate, w_up, w_down,
+                                               w_gate_up_t_packed, w_down_t_packed, stream),
                     "llep_pack_weights_backward");
 }
 
 size_t llep_grouped_ffn_backward_workspace_bytes(const llep_plan_params *params, int32_t D,
                                                  int32_t F, llep_dtype dtype) {
-  if (check_params(params) != LLEP_OK || D < 1 || F < 1 || dtype != LLEP_BF16) return 0;
-  return llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F);
+  if (check_params(params) != LLEP_OK || D < 1 || F < 1 || elem_bytes(dtype) == 0) return 0;
+  return llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F,
+                                            dtype);
 }
 
 int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_buffers *plan,
@@ -292,7 +292,6 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
   if (rc != LLEP_OK) return rc;
   if ((rc = check_plan_buffers(plan)) != LLEP_OK) return rc;
   if ((rc = check_ffn_dims(D, F, dtype)) != LLEP_OK) return rc;
-  if (dtype != LLEP_BF16) return fail(LLEP_E_DTYPE, "the backward supports bf16 only");
   if (device < -1 || device >= params->P) return fail(LLEP_E_ARG, "device outside [-1, P)");
   if (!x_perm || !d_out_perm || !w_gate_up_packed || !w_gate_up_t_packed || !w_down_t_packed ||
       !dx_perm || !dw_gate || !dw_up || !dw_down)
@@ -302,7 +301,7 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
       !aligned16(dw_gate) || !aligned16(dw_up) || !aligned16(dw_down))
     return fail(LLEP_E_ARG, "data not 16-byte aligned");
   const size_t need =
-      llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F);
+      llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F, dtype);
   if (!workspace || workspace_bytes < need)
     return fail(LLEP_E_WORKSPACE,
                 "workspace missing or smaller than llep_grouped_ffn_backward_workspace_bytes");
@@ -315,6 +314,7 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
   a.D = D;
   a.F = F;
   a.device = device;
+  a.dtype = dtype;
   a.groups = plan->groups;
   a.group_begin = plan->group_begin;
   a.x_perm = x_perm;

@@ -1146,7 +1146,15 @@ static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t 
   return L;
 }
 
-size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F) {
+// float32 path: [d g | d u] (gate / up interleaved per 32 like the packed
+// [Wg | Wu]) and the activation, per x_perm row
+static size_t f32_bwd_bytes(int64_t R, int32_t F) {
+  return 256 + round256(size_t(R) * 3 * F * 4);
+}
+
+size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F,
+                                    llep_dtype dtype) {
+  if (dtype == LLEP_F32) return f32_bwd_bytes(R, F);
   return bwd_layout(R, E, P, D, F).total;
 }
 
@@ -1270,17 +1278,151 @@ __global__ __launch_bounds__(256) void pack_bwd_kernel(const T *__restrict__ wg,
   }
 }
 
-hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, const void *w_gate,
+hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const void *w_gate,
                                 const void *w_up, const void *w_down, void *gut, void *dnt,
                                 hipStream_t stream) {
-  hipLaunchKernelGGL(pack_bwd_kernel<uint16_t>, dim3(4096), dim3(256), 0, stream,
-                     static_cast<const uint16_t *>(w_gate), static_cast<const uint16_t *>(w_up),
-                     static_cast<const uint16_t *>(w_down), static_cast<uint16_t *>(gut),
-                     static_cast<uint16_t *>(dnt), E, D, F);
+  if (dtype == LLEP_F32)
+    hipLaunchKernelGGL(pack_bwd_kernel<float>, dim3(4096), dim3(256), 0, stream,
+                       static_cast<const float *>(w_gate), static_cast<const float *>(w_up),
+                       static_cast<const float *>(w_down), static_cast<float *>(gut),
+                       static_cast<float *>(dnt), E, D, F);
+  else
+    hipLaunchKernelGGL(pack_bwd_kernel<uint16_t>, dim3(4096), dim3(256), 0, stream,
+                       static_cast<const uint16_t *>(w_gate), static_cast<const uint16_t *>(w_up),
+                       static_cast<const uint16_t *>(w_down), static_cast<uint16_t *>(gut),
+                       static_cast<uint16_t *>(dnt), E, D, F);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// float32 backward: one thread per output element (small layers; reference
+// precision, no matrix cores). Same operations and the same gradient-return
+// order as the bf16 path, without the bf16 roundings of the intermediates.
+// ---------------------------------------------------------------------------
+
+// per (row, f) of the range: g, u recomputed, d act = d out . Wd[f], then
+// d g, d u (into [row][2F], gate at 64 (f / 32) + f % 32, up 32 further) and
+// act = silu(g) u (into [row][F])
+__global__ __launch_bounds__(256) void ffn_f32_bwd_act_kernel(
+    const float *__restrict__ x_perm, const float *__restrict__ d_out_perm,
+    const float *__restrict__ wgu, const float *__restrict__ wdt, float *__restrict__ dgu,
+    float *__restrict__ act, const int32_t *__restrict__ groups,
+    const int32_t *__restrict__ group_begin, int32_t device, int32_t P, int32_t D, int32_t F) {
+  int lo, hi, row_first, rows;
+  device_range(groups, group_begin, device, P, lo, hi, row_first, rows);
+  const int64_t total = int64_t(rows) * F;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < total;
+       u += int64_t(gridDim.x) * blockDim.x) {
+    const int row = row_first + int(u / F), f = int(u % F);
+    const int e = groups[4 * group_of_row(groups, lo, hi, row) + 1];
+    const float *xr = x_perm + int64_t(row) * D;
+    const float *dor = d_out_perm + int64_t(row) * D;
+    const int pg = 64 * (f / 32) + (f % 32);
+    const float *we = wgu + int64_t(e) * 2 * F * D;
+    const float *wd = wdt + int64_t(e) * F * D;
+    float gs = 0.0f, us = 0.0f, da = 0.0f;
+    for (int d = 0; d < D; ++d) {
+      gs = fmaf(xr[d], we[packed_index(pg, d, D)], gs);
+      us = fmaf(xr[d], we[packed_index(pg + 32, d, D)], us);
+      da = fmaf(dor[d], wd[packed_index(f, d, D)], da);
+    }
+    const float sg = 1.0f / (1.0f + expf(-gs));
+    dgu[int64_t(row) * 2 * F + pg] = da * us * (sg * (1.0f + gs * (1.0f - sg)));
+    dgu[int64_t(row) * 2 * F + pg + 32] = da * gs * sg;
+    act[int64_t(row) * F + f] = gs * sg * us;
+  }
+}
+
+// per (row, d) of the range: dX = [d g | d u] . [Wg | Wu] row d
+__global__ __launch_bounds__(256) void ffn_f32_bwd_dx_kernel(
+    const float *__restrict__ dgu, const float *__restrict__ wgut, float *__restrict__ dx,
+    const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
+    int32_t P, int32_t D, int32_t F) {
+  int lo, hi, row_first, rows;
+  device_range(groups, group_begin, device, P, lo, hi, row_first, rows);
+  const int64_t total = int64_t(rows) * D;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < total;
+       u += int64_t(gridDim.x) * blockDim.x) {
+    const int row = row_first + int(u / D), c = int(u % D);
+    const int e = groups[4 * group_of_row(groups, lo, hi, row) + 1];
+    const float *gr = dgu + int64_t(row) * 2 * F;
+    const float *we = wgut + int64_t(e) * 2 * F * D;
+    float s = 0.0f;
+    for (int j = 0; j < 2 * F; ++j) s = fmaf(gr[j], we[packed_index(c, j, 2 * F)], s);
+    dx[int64_t(row) * D + c] = s;
+  }
+}
+
+// per (expert, m, n) of the three weight gradients: the sum over the
+// expert's groups of the range in gradient-return order (the group on the
+// expert's native device first, then the others by increasing device), rows
+// in order. Which = 0: dWg[e][d][f] (X^T d g), 1: dWu, 2: dWd[e][f][d]
+// (act^T d out). Experts without a group in the range are not written.
+__global__ __launch_bounds__(256) void ffn_f32_bwd_wgrad_kernel(
+    const float *__restrict__ x_perm, const float *__restrict__ d_out_perm,
+    const float *__restrict__ dgu, const float *__restrict__ act, float *__restrict__ dwg,
+    float *__restrict__ dwu, float *__restrict__ dwd, const int32_t *__restrict__ groups,
+    const int32_t *__restrict__ group_begin, int32_t device, int32_t P, int32_t E, int32_t M,
+    int32_t D, int32_t F) {
+  const int lo = device < 0 ? group_begin[0] : group_begin[device];
+  const int hi = device < 0 ? group_begin[P] : group_begin[device + 1];
+  const int64_t per = int64_t(D) * F, total = 3 * int64_t(E) * per;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < total;
+       u += int64_t(gridDim.x) * blockDim.x) {
+    const int which = int(u / (int64_t(E) * per));
+    const int64_t rem = u % (int64_t(E) * per);
+    const int e = int(rem / per);
+    const int64_t o = rem % per;
+    // dWg, dWu: element (d, f); dWd: element (f, d)
+    const int a = which < 2 ? int(o / F) : int(o / D);  // d, or f for dWd
+    const int b = which < 2 ? int(o % F) : int(o % D);  // f, or d for dWd
+    float s = 0.0f;
+    bool any = false;
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int gi = lo; gi < hi; ++gi) {
+        const int32_t *gr = groups + 4 * gi;
+        if (gr[1] != e || (gr[0] == e / M) != (pass == 0)) continue;
+        any = true;
+        for (int r = gr[2]; r < gr[2] + gr[3]; ++r) {
+          if (which == 0)
+            s = fmaf(x_perm[int64_t(r) * D + a], dgu[int64_t(r) * 2 * F + 64 * (b / 32) + b % 32], s);
+          else if (which == 1)
+            s = fmaf(x_perm[int64_t(r) * D + a],
+                     dgu[int64_t(r) * 2 * F + 64 * (b / 32) + b % 32 + 32], s);
+          else
+            s = fmaf(act[int64_t(r) * F + a], d_out_perm[int64_t(r) * D + b], s);
+        }
+      }
+    }
+    if (!any) continue;
+    float *dst = which == 0 ? dwg : which == 1 ? dwu : dwd;
+    dst[int64_t(e) * per + o] = s;
+  }
+}
+
+static hipError_t launch_grouped_ffn_backward_f32(const FfnBwdArgs &a, hipStream_t stream) {
+  float *dgu = reinterpret_cast<float *>(static_cast<char *>(a.ws) + 256);
+  float *act = dgu + size_t(a.R) * 2 * a.F;
+  const int grid = 4096;
+  hipLaunchKernelGGL(ffn_f32_bwd_act_kernel, dim3(grid), dim3(256), 0, stream,
+                     static_cast<const float *>(a.x_perm), static_cast<const float *>(a.d_out_perm),
+                     static_cast<const float *>(a.w_gate_up), static_cast<const float *>(a.w_down_t),
+                     dgu, act, a.groups, a.group_begin, a.device, a.P, a.D, a.F);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(ffn_f32_bwd_dx_kernel, dim3(grid), dim3(256), 0, stream, dgu,
+                     static_cast<const float *>(a.w_gate_up_t), static_cast<float *>(a.dx_perm),
+                     a.groups, a.group_begin, a.device, a.P, a.D, a.F);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  hipLaunchKernelGGL(ffn_f32_bwd_wgrad_kernel, dim3(grid), dim3(256), 0, stream,
+                     static_cast<const float *>(a.x_perm), static_cast<const float *>(a.d_out_perm),
+                     dgu, act, a.dw_gate, a.dw_up, a.dw_down, a.groups, a.group_begin, a.device,
+                     a.P, a.E, a.E / a.P, a.D, a.F);
   return hipGetLastError();
 }
 
 hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) {
+  if (a.dtype == LLEP_F32) return launch_grouped_ffn_backward_f32(a, stream);
   const BwdLayout L = bwd_layout(a.R, a.E, a.P, a.D, a.F);
   char *ws = static_cast<char *>(a.ws);
   int32_t *n_mtiles = reinterpret_cast<int32_t *>(ws);

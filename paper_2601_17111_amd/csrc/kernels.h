@@ -79,21 +79,24 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream);
 struct FfnBwdArgs {
   int64_t R;
   int32_t P, E, D, F, device;
+  llep_dtype dtype;
   const int32_t *groups, *group_begin;
   const void *x_perm, *d_out_perm, *w_gate_up, *w_gate_up_t, *w_down_t;
   void *dx_perm;
   float *dw_gate, *dw_up, *dw_down;
   void *ws;
 };
-size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F);
+size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F,
+                                    llep_dtype dtype);
 hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream);
-hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, const void *w_gate,
+hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const void *w_gate,
                                 const void *w_up, const void *w_down, void *gut, void *dnt,
                                 hipStream_t stream);
 
 struct CombineBwdArgs {
   int64_t T;
   int32_t K, D;
+  llep_dtype dtype;
   const void *out_perm, *dy;
   const int32_t *pair_row;
   const float *gates;

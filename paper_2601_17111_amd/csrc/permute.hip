@@ -375,7 +375,7 @@ hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
 // ---------------------------------------------------------------------------
 // Backward of the combine (Eq. 1). For every valid pair (t, k) with row
 // r = pair_row[t*K + k]:
-//   d_out_perm[r] = gates[t, k] * dy[t]              (one rounding)
+//   d_out_perm[r] = gates[t, k] * dy[t]              (one rounding to bf16)
 //   d_gates[t, k] = sum_i dy[t, i] * out_perm[r, i]  (float32)
 // and d_gates = 0 for pairs without a row. One wavefront per token; the
 // token's dy slice is held in registers while the pairs' rows stream past.
@@ -387,7 +387,7 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-template <int kV>
+template <bool kBf16, int kV>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(
     const i32x4 *__restrict__ out_perm, const int32_t *__restrict__ pair_row,
     const float *__restrict__ gates, const i32x4 *__restrict__ dy, i32x4 *__restrict__ d_out_perm,
@@ -440,12 +440,18 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
               i32x4 o;
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
-                const uint32_t du = uint32_t(dv[b][i]), qu = uint32_t(q[j][b][i]);
-                const float d0 = __uint_as_float(du << 16), d1 = __uint_as_float(du & 0xffff0000u);
-                part = fmaf(d0, __uint_as_float(qu << 16), part);
-                part = fmaf(d1, __uint_as_float(qu & 0xffff0000u), part);
-                o[i] = int32_t(uint32_t(f32_to_bf16(g[j] * d0)) |
-                               (uint32_t(f32_to_bf16(g[j] * d1)) << 16));
+                if (kBf16) {
+                  const uint32_t du = uint32_t(dv[b][i]), qu = uint32_t(q[j][b][i]);
+                  const float d0 = __uint_as_float(du << 16), d1 = __uint_as_float(du & 0xffff0000u);
+                  part = fmaf(d0, __uint_as_float(qu << 16), part);
+                  part = fmaf(d1, __uint_as_float(qu & 0xffff0000u), part);
+                  o[i] = int32_t(uint32_t(f32_to_bf16(g[j] * d0)) |
+                                 (uint32_t(f32_to_bf16(g[j] * d1)) << 16));
+                } else {
+                  const float d0 = __int_as_float(dv[b][i]);
+                  part = fmaf(d0, __int_as_float(q[j][b][i]), part);
+                  o[i] = __float_as_int(g[j] * d0);
+                }
               }
               if (v < vecs) d_out_perm[int64_t(row[j]) * vecs + v] = o;
             }
@@ -459,28 +465,36 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
   }
 }
 
-template <int kV>
+template <bool kBf16, int kV>
 void launch_combine_bwd_v(int grid, hipStream_t stream, const CombineBwdArgs &a, int32_t vecs) {
-  hipLaunchKernelGGL((combine_bwd_kernel<kV>), dim3(grid), dim3(256), 0, stream,
+  hipLaunchKernelGGL((combine_bwd_kernel<kBf16, kV>), dim3(grid), dim3(256), 0, stream,
                      static_cast<const i32x4 *>(a.out_perm), a.pair_row, a.gates,
                      static_cast<const i32x4 *>(a.dy), static_cast<i32x4 *>(a.d_out_perm),
                      a.d_gates, a.T, a.K, vecs);
 }
 
+template <bool kBf16>
+void launch_combine_bwd_t(int grid, hipStream_t stream, const CombineBwdArgs &a, int32_t vecs) {
+  switch (vecs_per_lane(vecs, kCombineBwdMaxVecs)) {
+    case 1: launch_combine_bwd_v<kBf16, 1>(grid, stream, a, vecs); break;
+    case 2: launch_combine_bwd_v<kBf16, 2>(grid, stream, a, vecs); break;
+    case 3: launch_combine_bwd_v<kBf16, 3>(grid, stream, a, vecs); break;
+    case 4: launch_combine_bwd_v<kBf16, 4>(grid, stream, a, vecs); break;
+    case 5: launch_combine_bwd_v<kBf16, 5>(grid, stream, a, vecs); break;
+    default: launch_combine_bwd_v<kBf16, 6>(grid, stream, a, vecs); break;
+  }
+}
+
 hipError_t launch_combine_backward(const CombineBwdArgs &a, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;
-  const int32_t vecs = a.D / 8;  // bfloat16 rows
-  const int kv = vecs_per_lane(vecs, kCombineBwdMaxVecs);
+  const bool bf16 = a.dtype == LLEP_BF16;
+  const int32_t vecs = bf16 ? a.D / 8 : a.D / 4;  // 16-byte vectors per row
   const int64_t blocks = (a.T + 3) / 4;
   const int grid = int(blocks < 65536 ? blocks : 65536);
-  switch (kv) {
-    case 1: launch_combine_bwd_v<1>(grid, stream, a, vecs); break;
-    case 2: launch_combine_bwd_v<2>(grid, stream, a, vecs); break;
-    case 3: launch_combine_bwd_v<3>(grid, stream, a, vecs); break;
-    case 4: launch_combine_bwd_v<4>(grid, stream, a, vecs); break;
-    case 5: launch_combine_bwd_v<5>(grid, stream, a, vecs); break;
-    default: launch_combine_bwd_v<6>(grid, stream, a, vecs); break;
-  }
+  if (bf16)
+    launch_combine_bwd_t<true>(grid, stream, a, vecs);
+  else
+    launch_combine_bwd_t<false>(grid, stream, a, vecs);
   return hipGetLastError();
 }
 

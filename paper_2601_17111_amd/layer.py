@@ -65,7 +65,7 @@ class LLEPLayer:
 
     def backward(self, dy, gates, w_gate_up, w_gate_up_t, w_down_t, device: int = -1,
                  stream=None):
-        """Backward of forward() (bf16), reusing its plan, permutation and expert
+        """Backward of forward() (bf16 or f32), reusing its plan, permutation and expert
         outputs: combine backward -> grouped FFN backward (one device's groups,
         or all with -1) -> the pairs' input gradients summed per token.
 
@@ -85,7 +85,8 @@ class LLEPLayer:
             self.dw_gate = torch.empty((E, D, F), dtype=torch.float32, device=dev)
             self.dw_up = torch.empty((E, D, F), dtype=torch.float32, device=dev)
             self.dw_down = torch.empty((E, F, D), dtype=torch.float32, device=dev)
-            nbytes = B.llep_grouped_ffn_backward_workspace_bytes(self.params, D, F, B.LLEP_BF16)
+            code = B.LLEP_BF16 if self.dtype == torch.bfloat16 else B.LLEP_F32
+            nbytes = B.llep_grouped_ffn_backward_workspace_bytes(self.params, D, F, code)
             self.bwd_workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         for w in (self.dw_gate, self.dw_up, self.dw_down):
             w.zero_()

@@ -159,8 +159,8 @@ def test_backward_argument_checks():
     bufs = B.llep_plan_buffers(*[16 * (i + 1) for i in range(10)])
     a = ctypes.c_void_p(4096)
     bf = B.LLEP_BF16
-    # combine backward: bf16 only, nulls, alignment, D % 8
-    assert L.llep_combine_backward(ctypes.byref(p), a, a, a, a, 64, B.LLEP_F32, a, a,
+    # combine backward: dtype, nulls, alignment, D % 8
+    assert L.llep_combine_backward(ctypes.byref(p), a, a, a, a, 64, 5, a, a,
                                    None) == B.LLEP_E_DTYPE
     assert L.llep_combine_backward(ctypes.byref(p), a, a, None, a, 64, bf, a, a,
                                    None) == B.LLEP_E_ARG
@@ -170,11 +170,12 @@ def test_backward_argument_checks():
     # the forward combine accepts null gates (all ones) but not a null output
     assert L.llep_combine(ctypes.byref(p), a, a, None, 64, bf, None, None) == B.LLEP_E_ARG
     # backward packing
-    assert L.llep_pack_weights_backward(4, 64, 64, B.LLEP_F32, a, a, a, a, a, None) == B.LLEP_E_DTYPE
+    assert L.llep_pack_weights_backward(4, 64, 64, 5, a, a, a, a, a, None) == B.LLEP_E_DTYPE
     assert L.llep_pack_weights_backward(4, 64, 96, bf, a, a, a, a, a, None) == B.LLEP_E_ARG
     assert L.llep_pack_weights_backward(4, 64, 64, bf, a, a, a, None, a, None) == B.LLEP_E_ARG
     # grouped FFN backward
-    assert B.llep_grouped_ffn_backward_workspace_bytes(p, 64, 128, B.LLEP_F32) == 0
+    assert B.llep_grouped_ffn_backward_workspace_bytes(p, 64, 128, 5) == 0
+    assert B.llep_grouped_ffn_backward_workspace_bytes(p, 64, 128, B.LLEP_F32) > 0
     need = B.llep_grouped_ffn_backward_workspace_bytes(p, 64, 128, bf)
     # at least the recomputed gate/up values, their gradients and the activation
     assert need >= p.T * p.K * 128 * 2 * 5
@@ -184,7 +185,7 @@ def test_backward_argument_checks():
     def call(device, D, F, dtype, ws, nbytes, dw):
         return L.llep_grouped_ffn_backward(ctypes.byref(p), ctypes.byref(bufs), device, a, a, a, a,
                                            a, D, F, dtype, a, dw, a, a, ws, nbytes, None)
-    assert call(**dict(ok, dtype=B.LLEP_F32)) == B.LLEP_E_DTYPE
+    assert call(**dict(ok, dtype=5)) == B.LLEP_E_DTYPE
     assert call(**dict(ok, D=96)) == B.LLEP_E_ARG
     assert call(**dict(ok, device=4)) == B.LLEP_E_ARG
     assert call(**dict(ok, dw=None)) == B.LLEP_E_ARG

@@ -12,6 +12,7 @@ from gpu_util import LayerRun, device, rel_err
 pytestmark = pytest.mark.gpu
 
 TOL_BF16 = 2e-2
+TOL_F32 = 1e-5
 
 
 @pytest.fixture(scope="module")
@@ -28,7 +29,8 @@ def _cfg(name, alpha=(11, 10), routing=("hot", 0.7, 2), **shape):
 def _dy(cfg, seed, dev):
     import torch
     g = torch.Generator(device="cpu").manual_seed(1000 + seed)
-    return torch.randn(cfg.T, cfg.D, generator=g).to(torch.bfloat16).to(dev)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    return torch.randn(cfg.T, cfg.D, generator=g).to(dt).to(dev)
 
 
 class BwdRun(LayerRun):
@@ -48,14 +50,16 @@ class BwdRun(LayerRun):
         return [t.float().cpu().numpy() for t in out]
 
 
-def test_pack_weights_backward_layout(dev):
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_pack_weights_backward_layout(dev, dtype):
     """Every element of the backward packing sits where the header puts it."""
     import torch
     from paper_2601_17111_amd import binding as B
     E, D, F = 2, 128, 192
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     g = torch.Generator(device="cpu").manual_seed(5)
-    wg, wu = (torch.randn(E, D, F, generator=g).to(torch.bfloat16) for _ in range(2))
-    wd = torch.randn(E, F, D, generator=g).to(torch.bfloat16)
+    wg, wu = (torch.randn(E, D, F, generator=g).to(tdt) for _ in range(2))
+    wd = torch.randn(E, F, D, generator=g).to(tdt)
     gut, dnt = B.llep_pack_weights_backward(wg.to(dev), wu.to(dev), wd.to(dev))
     torch.cuda.synchronize()
     gut, dnt = gut.cpu().reshape(E, -1), dnt.cpu().reshape(E, -1)
@@ -95,14 +99,17 @@ def test_combine_backward_rows_and_gates(dev):
     assert np.allclose(got_g, want_g, rtol=1e-5, atol=1e-5 * np.abs(want_g).max())
 
 
-@pytest.mark.parametrize("T,K,D", [(37, 70, 4096), (200, 5, 136), (3, 4, 8), (50, 4, 2560),
-                                   (41, 6, 2880)])
-def test_combine_backward_standalone(dev, T, K, D):
+@pytest.mark.parametrize("T,K,D,dtype", [(37, 70, 4096, "bf16"), (200, 5, 136, "bf16"),
+                                         (3, 4, 8, "bf16"), (50, 4, 2560, "bf16"),
+                                         (41, 6, 2880, "bf16"), (37, 70, 2048, "f32"),
+                                         (200, 5, 72, "f32"), (3, 4, 8, "f32")])
+def test_combine_backward_standalone(dev, T, K, D, dtype):
     """Rows longer than one wave slice, rows of a ragged number of vectors,
-    K > 64 (two 64-pair batches), and an invalid pair."""
+    K > 64 (two 64-pair batches), and an invalid pair; bf16 and float32."""
     import torch
     from paper_2601_17111_amd import binding as B
     E, P = 8, 2
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     rng = np.random.default_rng(9 + D)
     ids = rng.integers(0, E, (T, K)).astype(np.int32)
     ids[min(5, T - 1), 3] = E + 1  # an invalid pair: no row, d gate 0
@@ -110,17 +117,17 @@ def test_combine_backward_standalone(dev, T, K, D):
     bufs = B.PlanBuffers(params, dev)
     ids_t = torch.from_numpy(ids).to(dev)
     gates = torch.from_numpy(rng.random((T, K)).astype(np.float32)).to(dev)
-    x = torch.randn(T, D, device=dev).to(torch.bfloat16)
+    x = torch.randn(T, D, device=dev).to(tdt)
     R = T * K
-    x_perm = torch.empty(R, D, dtype=torch.bfloat16, device=dev)
+    x_perm = torch.empty(R, D, dtype=tdt, device=dev)
     gp = torch.empty(R, dtype=torch.float32, device=dev)
     rp = torch.empty(R, dtype=torch.int32, device=dev)
     pr = torch.empty(R, dtype=torch.int32, device=dev)
     B.llep_plan(params, ids_t, bufs)
     B.llep_permute(params, bufs, ids_t, gates, x, x_perm, gp, rp, pr)
-    out_perm = torch.randn(R, D, device=dev).to(torch.bfloat16)
-    dy = torch.randn(T, D, device=dev).to(torch.bfloat16)
-    d_out = torch.zeros(R, D, dtype=torch.bfloat16, device=dev)
+    out_perm = torch.randn(R, D, device=dev).to(tdt)
+    dy = torch.randn(T, D, device=dev).to(tdt)
+    d_out = torch.zeros(R, D, dtype=tdt, device=dev)
     dg = torch.full((T, K), 7.0, device=dev)
     B.llep_combine_backward(params, out_perm, pr, gates, dy, d_out, dg)
     torch.cuda.synchronize()
@@ -137,7 +144,7 @@ def test_combine_backward_standalone(dev, T, K, D):
     assert np.allclose(got, want, rtol=1e-5, atol=1e-5 * np.abs(want).max())
     g = gates.cpu().numpy().reshape(-1)
     want_rows = (torch.from_numpy(g[valid]).reshape(-1, 1) *
-                 torch.from_numpy(np.repeat(d, K, 0)[valid]).float()).to(torch.bfloat16)
+                 torch.from_numpy(np.repeat(d, K, 0)[valid]).float()).to(tdt)
     assert torch.equal(d_out.cpu()[torch.from_numpy(prn[valid].astype(np.int64))], want_rows)
 
 
@@ -271,15 +278,46 @@ def test_backward_empty_and_single_rows(dev):
 
 
 def test_backward_rejects_bad_arguments(dev):
-    import torch
+    import ctypes
     from paper_2601_17111_amd import binding as B
     params = B.make_params(16, 2, 8, 4, 8)
-    assert B.llep_grouped_ffn_backward_workspace_bytes(params, 64, 64, B.LLEP_F32) == 0
+    assert B.llep_grouped_ffn_backward_workspace_bytes(params, 64, 64, 7) == 0
     assert B.llep_grouped_ffn_backward_workspace_bytes(params, 64, 64, B.LLEP_BF16) > 0
-    z = torch.zeros((8, 64, 64), dtype=torch.float32, device=dev)
-    with pytest.raises(B.LLEPError) as ei:
-        B.llep_pack_weights_backward(z, z, z)
-    assert ei.value.code == B.LLEP_E_DTYPE
+    a = ctypes.c_void_p(4096)
+    assert B.lib().llep_pack_weights_backward(8, 64, 64, 7, a, a, a, a, a, None) == B.LLEP_E_DTYPE
+
+
+def test_f32_backward_tiny_layer(dev):
+    """The float32 path on the tiny layer: input, gate and weight gradients
+    against the plan-free float64 gradients, and every device's partials
+    against the oracle's partials of the same plan, to 1e-5."""
+    from paper_2601_17111_amd.synth import CONFIGS
+    cfg = CONFIGS["tiny-fp32"]
+    run = BwdRun(cfg, 0, dev)
+    tot = [t.copy() for t in run.backward(-1)]
+    ids_flat = run.inp.ids.reshape(-1)
+    pl = oracle.plan(ids_flat.tolist(), cfg.E, cfg.P, cfg.capacity, cfg.min_chunk, lam=cfg.lam)
+    assert any(d != e // (cfg.E // cfg.P) for (d, e, _, _) in pl.groups)  # spilled chunks
+    _, row_pair = oracle.permute(ids_flat.tolist(), pl, cfg.E)
+    W = run.host_weights(range(cfg.E))
+    x = run.x.cpu().numpy()
+    dy = run.dy.cpu().numpy()
+    _, partials, dW = oracle.plan_backward(x, ids_flat, run.inp.gates.reshape(-1), lambda e: W[e],
+                                           dy, pl, np.asarray(row_pair), cfg.K, cfg.E // cfg.P)
+    want_dx, want_dg, want_dW = oracle.moe_backward(x, run.inp.ids, run.inp.gates,
+                                                    lambda e: W[e], dy, cfg.E)
+    assert rel_err(tot[0], want_dx) <= TOL_F32
+    assert rel_err(tot[1], want_dg) <= TOL_F32
+    for e in range(cfg.E):
+        for got, want in zip((tot[2][e], tot[3][e], tot[4][e]), want_dW[e]):
+            assert rel_err(got, want) <= TOL_F32, e
+    for d in range(cfg.P):
+        parts = run.backward(d)[2:]
+        for (dd, e), want in partials.items():
+            if dd != d:
+                continue
+            for got, w in zip((p[e] for p in parts), want):
+                assert rel_err(got, w) <= TOL_F32, (d, e)
 
 
 def test_backward_force_assign_plan(dev):
