@@ -130,50 +130,76 @@ def _time_steps(layer, run, steps, dstar):
 def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps):
     """The backward of the step on the most-loaded device's share: combine
     backward (all tokens) -> grouped SwiGLU backward of d*'s groups (input
-    gradients of its rows and its partial weight gradients) -> the pairs'
-    input gradients summed per token. HIP event times per segment (ms)."""
+    gradients of its rows and its partial weight gradients) from the gate /
+    up values the training forward kept -> the pairs' input gradients summed
+    per token. Also timed: the same backward recomputing gate / up, and the
+    training forward's grouped FFN on d* (which keeps them). HIP event times
+    per segment (ms)."""
     import torch
     from paper_2601_17111_amd import binding as B
     gut, dnt = B.llep_pack_weights_backward(wg, wu, wd)
     g = torch.Generator(device=run["x"].device)
     g.manual_seed(7)
     dy = torch.randn(cfg.T, cfg.D, generator=g, device=run["x"].device).to(torch.bfloat16)
-    layer.forward(run["ids"], run["gates"], run["x"], run["gu"], run["dn"], -1)
+    layer.forward(run["ids"], run["gates"], run["x"], run["gu"], run["dn"], -1,
+                  save_gate_up=True)
     layer.backward(dy, run["gates"], run["gu"], gut, dnt, dstar)  # allocates the buffers
     L = layer
 
-    def step():
+    def step(gate_up):
         B.llep_combine_backward(L.params, L.out_perm, L.pair_row, run["gates"], dy, L.d_out_perm,
                                 L.d_gates)
         e[1].record()
         B.llep_grouped_ffn_backward(L.params, L.bufs, dstar, L.x_perm, L.d_out_perm, run["gu"],
                                     gut, dnt, L.dx_perm, L.dw_gate, L.dw_up, L.dw_down,
-                                    L.bwd_workspace)
+                                    L.bwd_workspace, gate_up=gate_up)
         e[2].record()
         B.llep_combine(L.params, L.dx_perm, L.pair_row, None, L.dx)
 
-    seg = {"combine_backward": 0.0, "grouped_ffn_backward": 0.0, "dx_sum": 0.0}
+    def timed(gate_up):
+        nonlocal e
+        seg = {"combine_backward": 0.0, "grouped_ffn_backward": 0.0, "dx_sum": 0.0}
+        for i in range(steps + 2):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record()
+            step(gate_up)
+            e[3].record()
+            torch.cuda.synchronize()
+            if i >= 2:
+                for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
+                    seg[k] += a.elapsed_time(b) / steps
+        return seg
+
+    e = None
+    seg = timed(L.gate_up)
+    recompute_ms = timed(None)["grouped_ffn_backward"]
+    # the training forward's grouped FFN on d*: the inference one plus the
+    # stores of gate / up
+    train_ms = 0.0
     for i in range(steps + 2):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-        e[0].record()
-        step()
-        e[3].record()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        L.ffn(run["gu"], run["dn"], dstar, save_gate_up=True)
+        b.record()
         torch.cuda.synchronize()
         if i >= 2:
-            for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
-                seg[k] += a.elapsed_time(b) / steps
+            train_ms += a.elapsed_time(b) / steps
     D, F, T, K = cfg.D, cfg.F, cfg.T, cfg.K
     R = T * K
     t_ffn = seg["grouped_ffn_backward"] * 1e-3
     cb_bytes = T * D * 2 + 2 * R * D * 2 + 12 * R
     del gut, dnt
+    L.gate_up = None
     return {
         "ms_per_step": sum(seg.values()), "segments_ms": seg, "device": dstar, "rows": n_rows,
         # 12 D F per row: the backward of the three projections (twice the
-        # forward); 16 D F with the recomputed gate/up projection
+        # forward); recomputing gate / up adds 4 D F
         "grouped_ffn_backward_TFLOPs": 12.0 * D * F * n_rows / t_ffn / 1e12,
-        "grouped_ffn_backward_executed_TFLOPs": 16.0 * D * F * n_rows / t_ffn / 1e12,
-        "grouped_ffn_backward_frac": 16.0 * D * F * n_rows / t_ffn / 1e12 / PEAK_BF16_TFLOPS,
+        "grouped_ffn_backward_frac": 12.0 * D * F * n_rows / t_ffn / 1e12 / PEAK_BF16_TFLOPS,
+        "grouped_ffn_backward_recompute_ms": recompute_ms,
+        "grouped_ffn_backward_recompute_TFLOPs":
+            16.0 * D * F * n_rows / (recompute_ms * 1e-3) / 1e12,
+        "grouped_ffn_train_forward_ms": train_ms,
         "combine_backward_GBps": cb_bytes / (seg["combine_backward"] * 1e-3) / 1e9,
         "tokens_per_s": T / (sum(seg.values()) * 1e-3),
     }

@@ -18,7 +18,9 @@
  *                     build chunks)
  *   llep_grouped_ffn  grouped SwiGLU expert GEMMs for one device's groups
  *                     (Alg. 4 grouped GEMMs over native and foreign experts;
- *                     three-matrix SwiGLU expert of Sec. 5.1)
+ *                     three-matrix SwiGLU expert of Sec. 5.1);
+ *                     llep_grouped_ffn_train also keeps g and u for the
+ *                     backward
  *   llep_combine      gate-weighted sum of each token's K expert rows (Eq. 1;
  *                     Alg. 4 reverse_sort, reshape, sum over K)
  *
@@ -207,6 +209,23 @@ int llep_grouped_ffn(const llep_plan_params *params,
                      llep_dtype dtype, void *out_perm, void *workspace,
                      size_t workspace_bytes, hipStream_t stream);
 
+/* Step 4 for training: llep_grouped_ffn, which also stores the gate and up
+ * projections g = X Wg_e, u = X Wu_e of every row of the range (rounded to
+ * dtype, as they enter the activation) so that llep_grouped_ffn_backward
+ * need not recompute them. gate_up [T*K][2F] in dtype, row-major by x_perm
+ * row, gate and up interleaved per 32 columns as in w_gate_up_packed:
+ * g[:, 32j + c] at column 64j + c, u[:, 32j + c] at column 64j + 32 + c.
+ * Rows outside the range are not written. out_perm is bit-identical to
+ * llep_grouped_ffn's. gate_up non-null and 16-byte aligned.
+ * Errors: as llep_grouped_ffn. */
+int llep_grouped_ffn_train(const llep_plan_params *params,
+                           const llep_plan_buffers *plan, int32_t device,
+                           const void *x_perm, const void *w_gate_up_packed,
+                           const void *w_down_packed, int32_t D, int32_t F,
+                           llep_dtype dtype, void *out_perm, void *gate_up,
+                           void *workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
 /* Step 5. y[t] = sum over k = 0..K-1 (ascending) of
  *   topk_gates[t*K+k] * out_perm[pair_row[t*K+k]]
  * in float32, rounded once to dtype; pairs with pair_row < 0 are skipped.
@@ -255,7 +274,7 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
 /* Backward of step 4 for the groups of `device` (or of all devices when
  * device == -1). With X = x_perm[rows of a group (d, e, s, n)] and
  * dO = d_out_perm[same rows] (from llep_combine_backward):
- *   g = X Wg_e, u = X Wu_e (recomputed), dA = dO Wd_e^T,
+ *   g = X Wg_e, u = X Wu_e, dA = dO Wd_e^T,
  *   dg = dA * u * silu'(g), du = dA * silu(g), act = silu(g) * u
  *   dx_perm[rows] = dg Wg_e^T + du Wu_e^T               (dtype)
  * and, per expert e with groups in the range, the weight gradients in
@@ -269,7 +288,10 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
  * written. Weights are the llep_pack_weights (w_gate_up_packed) and
  * llep_pack_weights_backward outputs. bf16 uses matrix cores and rounds g,
  * u, dg, du and act to bf16 once each; f32 is a plain reference-precision
- * path (no intermediate rounding). Workspace of at least
+ * path (no intermediate rounding). g and u are read from gate_up when it
+ * is non-null (the llep_grouped_ffn_train output for the same plan, device
+ * range and x_perm; the results are then bit-identical to recomputing),
+ * else recomputed (one more grouped GEMM). Workspace of at least
  * llep_grouped_ffn_backward_workspace_bytes bytes, 256-byte aligned.
  * Requires D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */
@@ -281,7 +303,8 @@ int llep_grouped_ffn_backward(const llep_plan_params *params,
                               const void *x_perm, const void *d_out_perm,
                               const void *w_gate_up_packed,
                               const void *w_gate_up_t_packed,
-                              const void *w_down_t_packed, int32_t D, int32_t F,
+                              const void *w_down_t_packed, const void *gate_up,
+                              int32_t D, int32_t F,
                               llep_dtype dtype, void *dx_perm, float *dw_gate,
                               float *dw_up, float *dw_down, void *workspace,
                               size_t workspace_bytes, hipStream_t stream);

@@ -34,7 +34,7 @@ EXPORTED = [
     "llep_grouped_ffn_workspace_bytes", "llep_packed_gate_up_bytes",
     "llep_packed_down_bytes", "llep_last_error", "llep_combine_backward",
     "llep_pack_weights_backward", "llep_grouped_ffn_backward_workspace_bytes",
-    "llep_grouped_ffn_backward",
+    "llep_grouped_ffn_backward", "llep_grouped_ffn_train",
 ]
 
 
@@ -93,15 +93,17 @@ def lib() -> ctypes.CDLL:
             "llep_grouped_ffn_workspace_bytes": (sz, [pp, i32, ctypes.c_int]),
             "llep_grouped_ffn": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, i32, i32,
                                                 ctypes.c_int, _P, _P, sz, _P]),
+            "llep_grouped_ffn_train": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, i32, i32,
+                                                      ctypes.c_int, _P, _P, _P, sz, _P]),
             "llep_combine": (ctypes.c_int, [pp, _P, _P, _P, i32, ctypes.c_int, _P, _P]),
             "llep_combine_backward": (ctypes.c_int, [pp, _P, _P, _P, _P, i32, ctypes.c_int, _P,
                                                      _P, _P]),
             "llep_pack_weights_backward": (ctypes.c_int, [i32, i32, i32, ctypes.c_int, _P, _P,
                                                           _P, _P, _P, _P]),
             "llep_grouped_ffn_backward_workspace_bytes": (sz, [pp, i32, i32, ctypes.c_int]),
-            "llep_grouped_ffn_backward": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, _P, _P, i32,
-                                                         i32, ctypes.c_int, _P, _P, _P, _P, _P,
-                                                         sz, _P]),
+            "llep_grouped_ffn_backward": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, _P, _P, _P,
+                                                         i32, i32, ctypes.c_int, _P, _P, _P, _P,
+                                                         _P, sz, _P]),
             "llep_last_error": (ctypes.c_char_p, []),
         }
         for name, (res, args) in sigs.items():
@@ -249,6 +251,20 @@ def llep_grouped_ffn(params: llep_plan_params, bufs: PlanBuffers, device: int, x
                                   _stream(stream)), "llep_grouped_ffn")
 
 
+def llep_grouped_ffn_train(params: llep_plan_params, bufs: PlanBuffers, device: int, x_perm,
+                           w_gate_up, w_down, out_perm, gate_up, workspace, stream=None):
+    """llep_grouped_ffn that also keeps g and u ([T*K, 2F], interleaved per
+    32 columns) for llep_grouped_ffn_backward."""
+    D = x_perm.shape[-1]
+    F = w_down.shape[-1]
+    _check(lib().llep_grouped_ffn_train(ctypes.byref(params), ctypes.byref(bufs.struct), device,
+                                        _ptr(x_perm), _ptr(w_gate_up), _ptr(w_down), D, F,
+                                        _dtype_code(x_perm), _ptr(out_perm), _ptr(gate_up),
+                                        _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(),
+                                        _stream(stream)), "llep_grouped_ffn_train")
+
+
 def llep_combine(params: llep_plan_params, out_perm, pair_row, topk_gates, y, stream=None):
     _check(lib().llep_combine(ctypes.byref(params), _ptr(out_perm), _ptr(pair_row),
                               _ptr(topk_gates), out_perm.shape[-1], _dtype_code(out_perm),
@@ -280,12 +296,14 @@ def llep_pack_weights_backward(w_gate, w_up, w_down, stream=None):
 
 def llep_grouped_ffn_backward(params: llep_plan_params, bufs: PlanBuffers, device: int, x_perm,
                               d_out_perm, w_gate_up, w_gate_up_t, w_down_t, dx_perm, dw_gate,
-                              dw_up, dw_down, workspace, stream=None):
+                              dw_up, dw_down, workspace, stream=None, gate_up=None):
+    """gate_up: the llep_grouped_ffn_train output (None: recompute g and u)."""
     D = x_perm.shape[-1]
     F = w_down_t.shape[-2]
     _check(lib().llep_grouped_ffn_backward(
         ctypes.byref(params), ctypes.byref(bufs.struct), device, _ptr(x_perm), _ptr(d_out_perm),
-        _ptr(w_gate_up), _ptr(w_gate_up_t), _ptr(w_down_t), D, F, _dtype_code(x_perm),
+        _ptr(w_gate_up), _ptr(w_gate_up_t), _ptr(w_down_t), _ptr(gate_up), D, F,
+        _dtype_code(x_perm),
         _ptr(dx_perm), _ptr(dw_gate), _ptr(dw_up), _ptr(dw_down), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)),
         "llep_grouped_ffn_backward")

@@ -172,11 +172,11 @@ size_t llep_grouped_ffn_workspace_bytes(const llep_plan_params *params, int32_t 
   return llep::ffn_workspace_bytes(params->T * params->K, params->E, params->P, F, dtype);
 }
 
-int llep_grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *plan,
-                     int32_t device, const void *x_perm, const void *w_gate_up_packed,
-                     const void *w_down_packed, int32_t D, int32_t F, llep_dtype dtype,
-                     void *out_perm, void *workspace, size_t workspace_bytes,
-                     hipStream_t stream) {
+static int grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *plan,
+                       int32_t device, const void *x_perm, const void *w_gate_up_packed,
+                       const void *w_down_packed, int32_t D, int32_t F, llep_dtype dtype,
+                       void *out_perm, void *gate_up, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream, const char *name) {
   int rc = check_params(params);
   if (rc != LLEP_OK) return rc;
   if ((rc = check_plan_buffers(plan)) != LLEP_OK) return rc;
@@ -192,7 +192,7 @@ int llep_grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *pl
     return fail(LLEP_E_WORKSPACE, "workspace missing or smaller than llep_grouped_ffn_workspace_bytes");
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
     return fail(LLEP_E_WORKSPACE, "workspace not 256-byte aligned");
-  llep::FfnArgs a;
+  llep::FfnArgs a = {};
   a.R = params->T * params->K;
   a.P = params->P;
   a.E = params->E;
@@ -206,9 +206,31 @@ int llep_grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *pl
   a.w_gate_up = w_gate_up_packed;
   a.w_down = w_down_packed;
   a.out_perm = out_perm;
+  a.gate_up_out = gate_up;
   a.ws = workspace;
   a.ws_bytes = workspace_bytes;
-  return hip_result(llep::launch_grouped_ffn(a, stream), "llep_grouped_ffn");
+  return hip_result(llep::launch_grouped_ffn(a, stream), name);
+}
+
+int llep_grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *plan,
+                     int32_t device, const void *x_perm, const void *w_gate_up_packed,
+                     const void *w_down_packed, int32_t D, int32_t F, llep_dtype dtype,
+                     void *out_perm, void *workspace, size_t workspace_bytes,
+                     hipStream_t stream) {
+  return grouped_ffn(params, plan, device, x_perm, w_gate_up_packed, w_down_packed, D, F, dtype,
+                     out_perm, nullptr, workspace, workspace_bytes, stream, "llep_grouped_ffn");
+}
+
+int llep_grouped_ffn_train(const llep_plan_params *params, const llep_plan_buffers *plan,
+                           int32_t device, const void *x_perm, const void *w_gate_up_packed,
+                           const void *w_down_packed, int32_t D, int32_t F, llep_dtype dtype,
+                           void *out_perm, void *gate_up, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  if (!gate_up) return fail(LLEP_E_ARG, "gate_up is null");
+  if (!aligned16(gate_up)) return fail(LLEP_E_ARG, "gate_up not 16-byte aligned");
+  return grouped_ffn(params, plan, device, x_perm, w_gate_up_packed, w_down_packed, D, F, dtype,
+                     out_perm, gate_up, workspace, workspace_bytes, stream,
+                     "llep_grouped_ffn_train");
 }
 
 int llep_combine(const llep_plan_params *params, const void *out_perm, const int32_t *pair_row,
@@ -284,10 +306,10 @@ size_t llep_grouped_ffn_backward_workspace_bytes(const llep_plan_params *params,
 int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_buffers *plan,
                               int32_t device, const void *x_perm, const void *d_out_perm,
                               const void *w_gate_up_packed, const void *w_gate_up_t_packed,
-                              const void *w_down_t_packed, int32_t D, int32_t F,
-                              llep_dtype dtype, void *dx_perm, float *dw_gate, float *dw_up,
-                              float *dw_down, void *workspace, size_t workspace_bytes,
-                              hipStream_t stream) {
+                              const void *w_down_t_packed, const void *gate_up, int32_t D,
+                              int32_t F, llep_dtype dtype, void *dx_perm, float *dw_gate,
+                              float *dw_up, float *dw_down, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
   int rc = check_params(params);
   if (rc != LLEP_OK) return rc;
   if ((rc = check_plan_buffers(plan)) != LLEP_OK) return rc;
@@ -298,7 +320,7 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
     return fail(LLEP_E_ARG, "a data pointer is null");
   if (!aligned16(x_perm) || !aligned16(d_out_perm) || !aligned16(w_gate_up_packed) ||
       !aligned16(w_gate_up_t_packed) || !aligned16(w_down_t_packed) || !aligned16(dx_perm) ||
-      !aligned16(dw_gate) || !aligned16(dw_up) || !aligned16(dw_down))
+      !aligned16(dw_gate) || !aligned16(dw_up) || !aligned16(dw_down) || !aligned16(gate_up))
     return fail(LLEP_E_ARG, "data not 16-byte aligned");
   const size_t need =
       llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F, dtype);
@@ -307,7 +329,7 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
                 "workspace missing or smaller than llep_grouped_ffn_backward_workspace_bytes");
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
     return fail(LLEP_E_WORKSPACE, "workspace not 256-byte aligned");
-  llep::FfnBwdArgs a;
+  llep::FfnBwdArgs a = {};
   a.R = params->T * params->K;
   a.P = params->P;
   a.E = params->E;
@@ -322,6 +344,7 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
   a.w_gate_up = w_gate_up_packed;
   a.w_gate_up_t = w_gate_up_t_packed;
   a.w_down_t = w_down_t_packed;
+  a.gate_up = gate_up;
   a.dx_perm = dx_perm;
   a.dw_gate = dw_gate;
   a.dw_up = dw_up;

@@ -156,11 +156,15 @@ struct GemmArgs {
   const int4 *tiles;        // forward: (group, m-tile, padded first row, 0)
   const int32_t *n_mtiles;
   int32_t N, Kdim;
-  // SwiGLU backward: reads the recomputed gate / up values (blocked
-  // [padded rows][2F]); besides [d g | d u] in that layout (C) it writes
-  // [d g | d u] and the activation transposed into the weight-gradient
-  // layout: blocks of 16 columns x 32 rows over [columns][kmax], the rows of
-  // group g starting at kbase[g]
+  // forward SwiGLU, training: the raw gate / up values, row-major by x_perm
+  // row (ld = N, gate / up interleaved per 32 as in the packed weights);
+  // null: not written
+  uint16_t *gu_save;
+  // SwiGLU backward: reads the gate / up values (row-major by x_perm row,
+  // ld 2F, interleaved per 32); writes [d g | d u] blocked over padded rows
+  // (C) and [d g | d u] and the activation transposed into the
+  // weight-gradient layout: blocks of 16 columns x 32 rows over
+  // [columns][kmax], the rows of group g starting at kbase[g]
   const uint16_t *GU;
   uint16_t *dgu_t, *act_t;
   const int32_t *kbase;
@@ -668,6 +672,23 @@ void gemm256_kernel(GemmArgs g) {
                 make_uint2(pack2(hv[0], hv[1]), pack2(hv[2], hv[3]));
           }
         }
+        if (g.gu_save) {
+          // raw gate and up values of this wave's rows, 4 columns per lane
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            if (i * 32 + (lane & 31) >= rows_w) continue;
+            uint16_t *gr = g.gu_save +
+                           int64_t(c.row0 + c.m0 + wm * WM + i * 32 + (lane & 31)) * g.N + pc;
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+              const f32x16 &ga = acc[i][2 * p], &ua = acc[i][2 * p + 1];
+              *reinterpret_cast<uint2 *>(gr + 8 * gq + 4 * h) =
+                  make_uint2(pack2(ga[4 * gq], ga[4 * gq + 1]), pack2(ga[4 * gq + 2], ga[4 * gq + 3]));
+              *reinterpret_cast<uint2 *>(gr + 32 + 8 * gq + 4 * h) =
+                  make_uint2(pack2(ua[4 * gq], ua[4 * gq + 1]), pack2(ua[4 * gq + 2], ua[4 * gq + 3]));
+            }
+          }
+        }
         // block rb of this wave = activation row block (prow0 + m0 + wm WM) / 16 + rb
         char *dst = reinterpret_cast<char *>(g.C) + (rb0 * (g.ldc >> 5) + (pc >> 6)) * 1024 +
                     lane * 16;
@@ -706,8 +727,8 @@ void gemm256_kernel(GemmArgs g) {
         }
       }
     } else if constexpr (kEpi == kEpiSwigluBwd) {
-      // C = d act for activation columns f. With g = gate, u = up
-      // (recomputed, blocked [padded rows][2F], gate f at column
+      // C = d act for activation columns f. With g = gate, u = up (saved by
+      // the forward or recomputed; row-major by x_perm row, gate f at column
       // 64 (f / 32) + f % 32, up 32 further): d gate = d act u silu'(g) and
       // d up = d act silu(g) go to C in the same layout (for dX), and d gate,
       // d up and act = silu(g) u go transposed to the weight-gradient layout:
@@ -728,7 +749,12 @@ void gemm256_kernel(GemmArgs g) {
       auto block_ok = [&](int i, int j) {
         return i * 32 < rows_w && c.n0 + wn * WN + j * 32 < g.N;
       };
-      auto gu_index = [&](int i, int j) {
+      auto gu_index = [&](int i, int j) {  // gate column 2 col0 of the lane's row
+        const int row = c.row0 + c.m0 + wm * WM + i * 32 + (lane & 31);
+        const int col0 = c.n0 + wn * WN + j * 32;
+        return int64_t(row) * (2 * F) + 2 * col0;
+      };
+      auto dgu_index = [&](int i, int j) {  // blocked [padded rows][2F]
         const int pr = c.prow0 + c.m0 + wm * WM + i * 32 + (lane & 31);
         const int col0 = c.n0 + wn * WN + j * 32;
         return (int64_t(pr >> 4) * gu_blocks + (col0 >> 5) * 2) * 512 + (pr & 15) * 32;
@@ -740,7 +766,7 @@ void gemm256_kernel(GemmArgs g) {
         for (int gq = 0; gq < 4; ++gq) {
           const int cc = 8 * gq + 4 * h;
           gw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + cc) : make_uint2(0u, 0u);
-          uw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + 512 + cc) : make_uint2(0u, 0u);
+          uw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + 32 + cc) : make_uint2(0u, 0u);
         }
       };
       uint2 gcur[4], ucur[4], gnxt[4], unxt[4];
@@ -754,7 +780,7 @@ void gemm256_kernel(GemmArgs g) {
           const bool row_ok = i * 32 + (lane & 31) < rows_w;
           const int64_t kb = (kb_grp + rr) >> 5;
           const int col0 = c.n0 + wn * WN + j * 32;  // first activation column f
-          const int64_t gblk = gu_index(i, j);
+          const int64_t gblk = dgu_index(i, j);
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
             const int cc = 8 * gq + 4 * h;  // column inside the 32-block
@@ -937,8 +963,8 @@ __device__ __forceinline__ int group_of_row(const int32_t *groups, int lo, int h
 
 __global__ __launch_bounds__(256) void ffn_f32_gate_up_kernel(
     const float *__restrict__ x_perm, const float *__restrict__ wgu, float *__restrict__ act,
-    const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
-    int32_t P, int32_t D, int32_t F) {
+    float *__restrict__ gu_save, const int32_t *__restrict__ groups,
+    const int32_t *__restrict__ group_begin, int32_t device, int32_t P, int32_t D, int32_t F) {
   int lo, hi, row_first, rows;
   device_range(groups, group_begin, device, P, lo, hi, row_first, rows);
   const int64_t total = int64_t(rows) * F;
@@ -955,6 +981,10 @@ __global__ __launch_bounds__(256) void ffn_f32_gate_up_kernel(
       us = fmaf(xr[d], we[packed_index(pg + 32, d, D)], us);
     }
     act[int64_t(row) * F + f] = gs / (1.0f + expf(-gs)) * us;
+    if (gu_save) {
+      gu_save[int64_t(row) * 2 * F + pg] = gs;
+      gu_save[int64_t(row) * 2 * F + pg + 32] = us;
+    }
   }
 }
 
@@ -1013,12 +1043,14 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
     g1.n_mtiles = n_mtiles;
     g1.N = 2 * a.F;
     g1.Kdim = a.D;
+    g1.gu_save = static_cast<uint16_t *>(a.gate_up_out);
     constexpr int NT = 64 * kWavesM * kWavesN;
     hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiSwiglu, false, true>),
                        dim3(grid), dim3(NT), 0, stream, g1);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g2 = g1;
+    g2.gu_save = nullptr;
     g2.A = static_cast<const uint16_t *>(act);
     g2.lda = a.F;
     g2.a_blk_stride = int64_t(a.F / kSK) * 1024;
@@ -1040,7 +1072,8 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
   }
   hipLaunchKernelGGL(ffn_f32_gate_up_kernel, dim3(1024), dim3(256), 0, stream,
                      static_cast<const float *>(a.x_perm), static_cast<const float *>(a.w_gate_up),
-                     static_cast<float *>(act), a.groups, a.group_begin, a.device, a.P, a.D, a.F);
+                     static_cast<float *>(act), static_cast<float *>(a.gate_up_out), a.groups,
+                     a.group_begin, a.device, a.P, a.D, a.F);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(ffn_f32_down_kernel, dim3(1024), dim3(256), 0, stream,
@@ -1136,7 +1169,7 @@ static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t 
   L.wge_off = o;    o = round256(o + size_t(E) * 16);
   L.kbase_off = o;  o = round256(o + size_t(L.max_groups) * 4);
   L.chunk_off = o;  o = round256(o + size_t(L.kmax / 32) * 4);
-  L.gu_off = o;     o = round256(o + size_t(L.prow_max) * 2 * F * 2);
+  L.gu_off = o;     o = round256(o + size_t(R) * 2 * F * 2);  // by x_perm row
   L.dgu_off = o;    o = round256(o + size_t(L.prow_max) * 2 * F * 2);
   L.xt_off = o;     o = round256(o + size_t(D) * L.kmax * 2);
   L.dot_off = o;    o = round256(o + size_t(D) * L.kmax * 2);
@@ -1305,7 +1338,8 @@ hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtyp
 // act = silu(g) u (into [row][F])
 __global__ __launch_bounds__(256) void ffn_f32_bwd_act_kernel(
     const float *__restrict__ x_perm, const float *__restrict__ d_out_perm,
-    const float *__restrict__ wgu, const float *__restrict__ wdt, float *__restrict__ dgu,
+    const float *__restrict__ gu_saved, const float *__restrict__ wgu,
+    const float *__restrict__ wdt, float *__restrict__ dgu,
     float *__restrict__ act, const int32_t *__restrict__ groups,
     const int32_t *__restrict__ group_begin, int32_t device, int32_t P, int32_t D, int32_t F) {
   int lo, hi, row_first, rows;
@@ -1322,9 +1356,15 @@ __global__ __launch_bounds__(256) void ffn_f32_bwd_act_kernel(
     const float *wd = wdt + int64_t(e) * F * D;
     float gs = 0.0f, us = 0.0f, da = 0.0f;
     for (int d = 0; d < D; ++d) {
-      gs = fmaf(xr[d], we[packed_index(pg, d, D)], gs);
-      us = fmaf(xr[d], we[packed_index(pg + 32, d, D)], us);
+      if (!gu_saved) {
+        gs = fmaf(xr[d], we[packed_index(pg, d, D)], gs);
+        us = fmaf(xr[d], we[packed_index(pg + 32, d, D)], us);
+      }
       da = fmaf(dor[d], wd[packed_index(f, d, D)], da);
+    }
+    if (gu_saved) {
+      gs = gu_saved[int64_t(row) * 2 * F + pg];
+      us = gu_saved[int64_t(row) * 2 * F + pg + 32];
     }
     const float sg = 1.0f / (1.0f + expf(-gs));
     dgu[int64_t(row) * 2 * F + pg] = da * us * (sg * (1.0f + gs * (1.0f - sg)));
@@ -1406,8 +1446,9 @@ static hipError_t launch_grouped_ffn_backward_f32(const FfnBwdArgs &a, hipStream
   const int grid = 4096;
   hipLaunchKernelGGL(ffn_f32_bwd_act_kernel, dim3(grid), dim3(256), 0, stream,
                      static_cast<const float *>(a.x_perm), static_cast<const float *>(a.d_out_perm),
-                     static_cast<const float *>(a.w_gate_up), static_cast<const float *>(a.w_down_t),
-                     dgu, act, a.groups, a.group_begin, a.device, a.P, a.D, a.F);
+                     static_cast<const float *>(a.gate_up), static_cast<const float *>(a.w_gate_up),
+                     static_cast<const float *>(a.w_down_t), dgu, act, a.groups, a.group_begin,
+                     a.device, a.P, a.D, a.F);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(ffn_f32_bwd_dx_kernel, dim3(grid), dim3(256), 0, stream, dgu,
@@ -1457,7 +1498,8 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   constexpr int NT192 = 64 * kWavesM192 * kWavesN192;
   const bool d192 = D % 256 != 0 && D % 192 == 0;
   const bool f192 = F % 256 != 0 && F % 192 == 0;
-  // 1. g, u = X [Wg | Wu] (interleaved per 32), blocked over padded rows
+  // 1. g, u = X [Wg | Wu] (interleaved per 32), row-major by x_perm row,
+  // unless the forward saved them
   GemmArgs g = {};
   g.A = static_cast<const uint16_t *>(a.x_perm);
   g.lda = D;
@@ -1471,9 +1513,11 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   g.n_mtiles = n_mtiles;
   g.N = 2 * F;
   g.Kdim = D;
-  hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, false, true>), dim3(grid),
-                     dim3(NT), 0, stream, g);
-  LLEP_CHECK_LAUNCH();
+  if (!a.gate_up) {
+    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiPlain, false, false>),
+                       dim3(grid), dim3(NT), 0, stream, g);
+    LLEP_CHECK_LAUNCH();
+  }
   // 2. d act = d out Wd^T; the epilogue writes [d g | d u] blocked (for dX)
   // and [d g | d u], act transposed into the weight-gradient layout
   GemmArgs g2 = g;
@@ -1486,7 +1530,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   g2.ldc = F;
   g2.N = F;
   g2.Kdim = D;
-  g2.GU = gu;
+  g2.GU = a.gate_up ? static_cast<const uint16_t *>(a.gate_up) : gu;
   g2.dgu_t = dgut;
   g2.act_t = actt;
   g2.kbase = kbase;

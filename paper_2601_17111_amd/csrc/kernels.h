@@ -69,6 +69,7 @@ struct FfnArgs {
   const int32_t *groups, *group_begin;
   const void *x_perm, *w_gate_up, *w_down;
   void *out_perm;
+  void *gate_up_out;  // training forward: raw gate / up values per x_perm row; null: none
   void *ws;
   size_t ws_bytes;
 };
@@ -82,6 +83,7 @@ struct FfnBwdArgs {
   llep_dtype dtype;
   const int32_t *groups, *group_begin;
   const void *x_perm, *d_out_perm, *w_gate_up, *w_gate_up_t, *w_down_t;
+  const void *gate_up;  // saved by the training forward; null: recompute
   void *dx_perm;
   float *dw_gate, *dw_up, *dw_down;
   void *ws;

@@ -46,28 +46,47 @@ class LLEPLayer:
         B.llep_permute(self.params, self.bufs, ids, gates, x, self.x_perm, self.gate_perm,
                        self.row_pair, self.pair_row, stream)
 
-    def ffn(self, w_gate_up, w_down, device: int = -1, stream=None):
-        B.llep_grouped_ffn(self.params, self.bufs, device, self.x_perm, w_gate_up, w_down,
-                           self.out_perm, self.workspace, stream)
+    def ffn(self, w_gate_up, w_down, device: int = -1, stream=None, save_gate_up=False):
+        """save_gate_up: keep g and u (self.gate_up) so that backward() does
+        not recompute them."""
+        if save_gate_up:
+            if getattr(self, "gate_up", None) is None:
+                import torch
+                self.gate_up = torch.empty((max(self.T * self.K, 1), 2 * self.F),
+                                           dtype=self.dtype, device=self.device)
+            B.llep_grouped_ffn_train(self.params, self.bufs, device, self.x_perm, w_gate_up,
+                                     w_down, self.out_perm, self.gate_up, self.workspace, stream)
+            self.gate_up_device = device
+        else:
+            B.llep_grouped_ffn(self.params, self.bufs, device, self.x_perm, w_gate_up, w_down,
+                               self.out_perm, self.workspace, stream)
+            self.gate_up_device = None
 
     def combine(self, gates, stream=None):
         B.llep_combine(self.params, self.out_perm, self.pair_row, gates, self.y, stream)
 
     def forward(self, ids, gates, x, w_gate_up, w_down, device: Optional[int] = -1,
-                stream=None):
+                stream=None, save_gate_up=False):
         """plan -> permute -> grouped FFN (one device's groups, or all with -1)
-        -> combine. Returns y (valid for every token only when device == -1)."""
+        -> combine. Returns y (valid for every token only when device == -1).
+        save_gate_up: training forward (g and u kept for backward())."""
         self.plan(ids, stream)
         self.permute(ids, gates, x, stream)
-        self.ffn(w_gate_up, w_down, -1 if device is None else device, stream)
+        self.ffn(w_gate_up, w_down, -1 if device is None else device, stream, save_gate_up)
         self.combine(gates, stream)
         return self.y
+
+    def _saved_covers(self, device: int) -> bool:
+        saved = getattr(self, "gate_up_device", None)
+        return saved is not None and (saved == -1 or saved == device)
 
     def backward(self, dy, gates, w_gate_up, w_gate_up_t, w_down_t, device: int = -1,
                  stream=None):
         """Backward of forward() (bf16 or f32), reusing its plan, permutation and expert
         outputs: combine backward -> grouped FFN backward (one device's groups,
-        or all with -1) -> the pairs' input gradients summed per token.
+        or all with -1) -> the pairs' input gradients summed per token. Uses
+        the g and u of a forward with save_gate_up (same device range), else
+        recomputes them.
 
         Returns (dx [T, D], d_gates [T, K] float32, dw_gate, dw_up [E, D, F],
         dw_down [E, F, D] float32). dx and d_gates cover every token only when
@@ -94,6 +113,7 @@ class LLEPLayer:
                                 self.d_out_perm, self.d_gates, stream)
         B.llep_grouped_ffn_backward(self.params, self.bufs, device, self.x_perm, self.d_out_perm,
                                     w_gate_up, w_gate_up_t, w_down_t, self.dx_perm, self.dw_gate,
-                                    self.dw_up, self.dw_down, self.bwd_workspace, stream)
+                                    self.dw_up, self.dw_down, self.bwd_workspace, stream,
+                                    self.gate_up if self._saved_covers(device) else None)
         B.llep_combine(self.params, self.dx_perm, self.pair_row, None, self.dx, stream)
         return self.dx, self.d_gates, self.dw_gate, self.dw_up, self.dw_down

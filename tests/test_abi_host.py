@@ -147,6 +147,16 @@ def test_ffn_argument_checks():
     assert call(**ok_args(nbytes=ws_need - 1)) == B.LLEP_E_WORKSPACE
     assert call(**ok_args(ws=None)) == B.LLEP_E_WORKSPACE
     assert call(**ok_args(ws=ctypes.c_void_p((1 << 20) + 128))) == B.LLEP_E_WORKSPACE
+
+    def train(gate_up, **kw):
+        k = ok_args(**kw)
+        return L.llep_grouped_ffn_train(ctypes.byref(p), ctypes.byref(bufs), k["device"], a, a, a,
+                                        k["D"], k["F"], k["dtype"], a, gate_up, k["ws"],
+                                        k["nbytes"], None)
+    assert train(None) == B.LLEP_E_ARG                    # gate_up required
+    assert train(ctypes.c_void_p(4104)) == B.LLEP_E_ARG   # misaligned
+    assert train(a, D=96) == B.LLEP_E_ARG
+    assert train(a, nbytes=ws_need - 1) == B.LLEP_E_WORKSPACE
     # pack
     assert L.llep_pack_weights(4, 64, 96, B.LLEP_BF16, a, a, a, a, a, None) == B.LLEP_E_ARG
     assert L.llep_pack_weights(0, 64, 64, B.LLEP_BF16, a, a, a, a, a, None) == B.LLEP_E_ARG
@@ -182,9 +192,9 @@ def test_backward_argument_checks():
     ws = ctypes.c_void_p(1 << 24)
     ok = dict(device=0, D=64, F=128, dtype=bf, ws=ws, nbytes=need, dw=a)
 
-    def call(device, D, F, dtype, ws, nbytes, dw):
+    def call(device, D, F, dtype, ws, nbytes, dw, gate_up=None):
         return L.llep_grouped_ffn_backward(ctypes.byref(p), ctypes.byref(bufs), device, a, a, a, a,
-                                           a, D, F, dtype, a, dw, a, a, ws, nbytes, None)
+                                           a, gate_up, D, F, dtype, a, dw, a, a, ws, nbytes, None)
     assert call(**dict(ok, dtype=5)) == B.LLEP_E_DTYPE
     assert call(**dict(ok, D=96)) == B.LLEP_E_ARG
     assert call(**dict(ok, device=4)) == B.LLEP_E_ARG
@@ -192,6 +202,7 @@ def test_backward_argument_checks():
     assert call(**dict(ok, dw=ctypes.c_void_p(4100))) == B.LLEP_E_ARG
     assert call(**dict(ok, nbytes=need - 1)) == B.LLEP_E_WORKSPACE
     assert call(**dict(ok, ws=ctypes.c_void_p((1 << 24) + 64))) == B.LLEP_E_WORKSPACE
+    assert call(**dict(ok, gate_up=ctypes.c_void_p(4104))) == B.LLEP_E_ARG
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -42,9 +42,11 @@ class BwdRun(LayerRun):
         self.dy = _dy(cfg, seed, dev)
         torch.cuda.synchronize()
 
-    def backward(self, device=-1):
+    def backward(self, device=-1, save=False, fwd_device=-1):
+        """save: training forward (g and u kept) over fwd_device's groups."""
         import torch
-        self.forward(-1)
+        self.layer.forward(self.ids, self.gates, self.x, self.gu, self.dn, fwd_device,
+                           save_gate_up=save)
         out = self.layer.backward(self.dy, self.gates, self.gu, self.gut, self.dnt, device)
         torch.cuda.synchronize()
         return [t.float().cpu().numpy() for t in out]
@@ -377,3 +379,75 @@ def test_backward_with_invalid_ids(dev):
     for e, want in want_dW.items():
         for got, w in zip((dwg[e], dwu[e], dwd[e]), want):
             assert rel_err(got, w) <= TOL_BF16, e
+
+
+@pytest.mark.parametrize("shape", SHAPES[:3], ids=lambda s: f"T{s['T']}D{s['D']}F{s['F']}E{s['E']}")
+def test_train_forward_saves_gate_up(dev, shape):
+    """The training forward gives the inference forward's bits and stores g
+    and u of exactly the rows of its device range, each within the bf16
+    tolerance of the float64 projections."""
+    import torch
+    cfg = _cfg("train-fwd", **shape)
+    run = BwdRun(cfg, 3, dev)
+    L = run.layer
+    run.forward(-1)
+    out_ref, y_ref = L.out_perm.clone(), L.y.clone()
+    L.gate_up = torch.full((cfg.T * cfg.K, 2 * cfg.F), float("nan"), dtype=torch.bfloat16,
+                           device=dev)
+    L.forward(run.ids, run.gates, run.x, run.gu, run.dn, -1, save_gate_up=True)
+    torch.cuda.synchronize()
+    total = int(L.bufs.device_rows.sum().item())
+    assert torch.equal(L.out_perm[:total], out_ref[:total])
+    assert torch.equal(L.y, y_ref)
+    gu = L.gate_up[:total].float().cpu().numpy()
+    assert np.isfinite(gu).all()
+    xp = L.x_perm[:total].float().cpu().numpy().astype(np.float64)
+    W = run.host_weights(range(cfg.E))
+    rows_expert = np.full(total, -1)
+    ng = L.bufs.info_dict()["n_groups"]
+    for (d, e, r0, n) in L.bufs.groups[:ng].cpu().tolist():
+        rows_expert[r0:r0 + n] = e
+    col = 32 * (np.arange(2 * cfg.F) // 64) + np.arange(2 * cfg.F) % 32
+    is_gate = np.arange(2 * cfg.F) % 64 < 32
+    for e in range(cfg.E):
+        rows = np.nonzero(rows_expert == e)[0]
+        if len(rows) == 0:
+            continue
+        wg, wu, _ = (w.astype(np.float64) for w in W[e])
+        want = np.where(is_gate, (xp[rows] @ wg)[:, col], (xp[rows] @ wu)[:, col])
+        assert rel_err(gu[rows], want) <= TOL_BF16, e
+    # one device's range: only its rows are written
+    rows = L.bufs.device_rows.cpu().tolist()
+    starts = np.concatenate([[0], np.cumsum(rows)])
+    d = int(np.argmax(rows))
+    L.gate_up.fill_(float("nan"))
+    L.forward(run.ids, run.gates, run.x, run.gu, run.dn, d, save_gate_up=True)
+    torch.cuda.synchronize()
+    a, b = int(starts[d]), int(starts[d + 1])
+    g2 = L.gate_up.float()
+    assert torch.isfinite(g2[a:b]).all()
+    assert torch.isnan(g2[:a]).all() and torch.isnan(g2[b:]).all()
+    assert np.array_equal(g2[a:b].cpu().numpy(), gu[a:b])
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_backward_from_saved_gate_up_is_bit_identical(dev, dtype):
+    """Backward from the training forward's g and u equals the backward that
+    recomputes them, bit for bit, for the whole layer and for one device's
+    range (saved by a forward over all devices or over that device)."""
+    from paper_2601_17111_amd.synth import CONFIGS
+    if dtype == "bf16":
+        cfg = _cfg("saved-gu", T=1000, D=256, F=320, E=16, K=4, P=4)
+    else:
+        cfg = CONFIGS["tiny-fp32"]
+    run = BwdRun(cfg, 8, dev)
+    ref = run.backward(-1)
+    got = run.backward(-1, save=True)
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+    d = 1
+    ref_d = run.backward(d)
+    for fwd in (-1, d):
+        got_d = run.backward(d, save=True, fwd_device=fwd)
+        for a, b in zip(got_d[2:], ref_d[2:]):
+            assert np.array_equal(a, b), fwd

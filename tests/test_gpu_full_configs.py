@@ -263,6 +263,15 @@ def test_full_backward(dev, name):
         den = tot.abs().max().item()
         assert (a - tot).abs().max().item() <= 1e-5 * den
     del acc
+    # training forward: the backward from the saved gate / up values gives
+    # the same bits as the one that recomputes them
+    L.forward(run.ids, run.gates, run.x, run.gu, run.dn, -1, save_gate_up=True)
+    saved = L.backward(dy_dev, run.gates, run.gu, gut, dnt, -1)
+    torch.cuda.synchronize()
+    for a, b in zip(saved, (dx, dg, dwg, dwu, dwd)):
+        assert torch.equal(a, b)
+    del saved
+    L.gate_up = None
     if name != "deepseek-v3":
         L.set_mode("ep")
         run.forward(-1)
