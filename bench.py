@@ -68,11 +68,38 @@ def _config(name):
     return CONFIGS[name]
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and blank space, so that the hash below
+    changes with the code only (string literals are kept as they are)."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == '"':
+            j = i + 1
+            while j < n and text[j] != '"':
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            while i < n and text[i] != "\n":
+                i += 1
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def _kernel_hash():
+    """Hash of the grouped-FFN kernel source (comments and spacing ignored):
+    the traffic figure is used only while the code it was measured on is
+    unchanged."""
     h = hashlib.sha256()
     for f in ("grouped_ffn.hip", "common.h"):
-        with open(os.path.join(ROOT, "paper_2601_17111_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2601_17111_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -125,8 +125,9 @@ __global__ __launch_bounds__(256) void tile_table_kernel(const int32_t *__restri
 // ---------------------------------------------------------------------------
 
 // Epilogues: the forward projections (plain bf16 C, or SwiGLU of gate/up
-// column pairs), the SwiGLU backward (C = d act; reads the recomputed gate /
-// up values, writes their gradients and the activation), and the backward's
+// column pairs; a training forward also stores the gate / up values), the
+// SwiGLU backward (C = d act; reads the gate / up values, writes their
+// gradients and the activation), and the backward's
 // multi-problem launch: the input-gradient tiles (plain bf16 C) together with
 // the tiles of the two weight gradients (fp32, per expert; gate/up columns
 // de-interleaved), handed out through a work counter.
@@ -1138,7 +1139,8 @@ hipError_t launch_pack(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const 
 // Backward of the grouped SwiGLU FFN (bf16), for the groups of one device or
 // of all devices. Given d out for the groups' rows (from the combine's
 // backward):
-//   1. recompute g, u = X [Wg | Wu]             (blocked over padded rows)
+//   1. g, u = X [Wg | Wu] (row-major by x_perm row), unless the training
+//      forward kept them
 //   2. d act = d out Wd^T; epilogue: d g, d u and act = silu(g) u
 //   3. dX = [d g | d u] [Wg | Wu]^T               (x_perm rows)
 //   4. weight gradients, in fp32 per expert: the rows of an expert's groups
@@ -1333,7 +1335,8 @@ hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtyp
 // order as the bf16 path, without the bf16 roundings of the intermediates.
 // ---------------------------------------------------------------------------
 
-// per (row, f) of the range: g, u recomputed, d act = d out . Wd[f], then
+// per (row, f) of the range: g, u (saved by the training forward, else
+// recomputed), d act = d out . Wd[f], then
 // d g, d u (into [row][2F], gate at 64 (f / 32) + f % 32, up 32 further) and
 // act = silu(g) u (into [row][F])
 __global__ __launch_bounds__(256) void ffn_f32_bwd_act_kernel(

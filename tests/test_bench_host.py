@@ -42,3 +42,16 @@ def test_flags_parse():
     assert bench._config(a.workload).E == 256
     # the committed traffic figure belongs to the default workload only
     assert bench._traffic("deepseek-v3") is None
+
+
+def test_kernel_hash_ignores_comments_only():
+    """The traffic figure is keyed by a hash of the GEMM source that ignores
+    comments and spacing but not code."""
+    sys.path.insert(0, ROOT)
+    import bench
+    a = bench._code_only('int x = 1;  // one\n/* two\n three */ int y = "//" [0];\n')
+    b = bench._code_only('int x = 1;\n\n   int y = "//" [0]; // other words\n')
+    c = bench._code_only('int x = 2;\nint y = "//" [0];\n')
+    assert a == b
+    assert a != c
+    assert '"//"' in a

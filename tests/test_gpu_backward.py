@@ -381,19 +381,22 @@ def test_backward_with_invalid_ids(dev):
             assert rel_err(got, w) <= TOL_BF16, e
 
 
-@pytest.mark.parametrize("shape", SHAPES[:3], ids=lambda s: f"T{s['T']}D{s['D']}F{s['F']}E{s['E']}")
+@pytest.mark.parametrize("shape", SHAPES[:3] + ["tiny-fp32"],
+                         ids=lambda s: s if isinstance(s, str) else
+                         f"T{s['T']}D{s['D']}F{s['F']}E{s['E']}")
 def test_train_forward_saves_gate_up(dev, shape):
     """The training forward gives the inference forward's bits and stores g
-    and u of exactly the rows of its device range, each within the bf16
+    and u of exactly the rows of its device range, each within the dtype's
     tolerance of the float64 projections."""
     import torch
-    cfg = _cfg("train-fwd", **shape)
+    from paper_2601_17111_amd.synth import CONFIGS
+    cfg = CONFIGS[shape] if isinstance(shape, str) else _cfg("train-fwd", **shape)
+    tol = TOL_BF16 if cfg.dtype == "bf16" else TOL_F32
     run = BwdRun(cfg, 3, dev)
     L = run.layer
     run.forward(-1)
     out_ref, y_ref = L.out_perm.clone(), L.y.clone()
-    L.gate_up = torch.full((cfg.T * cfg.K, 2 * cfg.F), float("nan"), dtype=torch.bfloat16,
-                           device=dev)
+    L.gate_up = torch.full((cfg.T * cfg.K, 2 * cfg.F), float("nan"), dtype=run.tdt, device=dev)
     L.forward(run.ids, run.gates, run.x, run.gu, run.dn, -1, save_gate_up=True)
     torch.cuda.synchronize()
     total = int(L.bufs.device_rows.sum().item())
@@ -415,7 +418,7 @@ def test_train_forward_saves_gate_up(dev, shape):
             continue
         wg, wu, _ = (w.astype(np.float64) for w in W[e])
         want = np.where(is_gate, (xp[rows] @ wg)[:, col], (xp[rows] @ wu)[:, col])
-        assert rel_err(gu[rows], want) <= TOL_BF16, e
+        assert rel_err(gu[rows], want) <= tol, e
     # one device's range: only its rows are written
     rows = L.bufs.device_rows.cpu().tolist()
     starts = np.concatenate([[0], np.cumsum(rows)])
