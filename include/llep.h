@@ -289,9 +289,11 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
  * llep_pack_weights_backward outputs. bf16 uses matrix cores and rounds g,
  * u, dg, du and act to bf16 once each; f32 is a plain reference-precision
  * path (no intermediate rounding). g and u are read from gate_up when it
- * is non-null (the llep_grouped_ffn_train output for the same plan, device
- * range and x_perm; the results are then bit-identical to recomputing),
- * else recomputed (one more grouped GEMM). Workspace of at least
+ * is non-null: the llep_grouped_ffn_train output for the same plan, x_perm
+ * and weights, over the same device or over all devices (-1); the results
+ * are then bit-identical to recomputing, and rows that call did not write
+ * give undefined gradients. Null gate_up: g and u are recomputed (one more
+ * grouped GEMM, into the workspace). Workspace of at least
  * llep_grouped_ffn_backward_workspace_bytes bytes, 256-byte aligned.
  * Requires D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */
