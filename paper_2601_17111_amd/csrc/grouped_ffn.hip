@@ -264,6 +264,16 @@ __device__ __forceinline__ int lds_swz32(int row, int kc) {
   return row * kSK + ((kc ^ ((row >> 2) & 3)) << 3);
 }
 
+// v_permlane32_swap: lanes 32..63 of `lo` trade places with lanes 0..31 of
+// `hi`. Lanes l and l + 32 of an accumulator block hold four columns each of
+// the same row, 4 apart; one swap per register pair turns them into eight
+// consecutive columns per lane, so a row's values move as 16-byte runs.
+__device__ __forceinline__ void swap_halves(uint32_t &lo, uint32_t &hi) {
+  const auto r = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+  lo = r[0];
+  hi = r[1];
+}
+
 struct TileCoord {
   int e, row0, prow0, m0, rows_valid, n0, cols_valid, k0, nk, grp;
   int p, N;  // problem (0: the main one, 1 / 2: wp[0] / wp[1]) and its columns
@@ -674,19 +684,29 @@ void gemm256_kernel(GemmArgs g) {
           }
         }
         if (g.gu_save) {
-          // raw gate and up values of this wave's rows, 4 columns per lane
+          // raw gate and up values of this wave's rows: after the half-wave
+          // swaps lane l stores columns 16 q + 0..7 of its row and lane
+          // l + 32 columns 16 q + 8..15
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
-            if (i * 32 + (lane & 31) >= rows_w) continue;
+            const bool row_ok = i * 32 + (lane & 31) < rows_w;
             uint16_t *gr = g.gu_save +
                            int64_t(c.row0 + c.m0 + wm * WM + i * 32 + (lane & 31)) * g.N + pc;
+            const f32x16 &ga = acc[i][2 * p], &ua = acc[i][2 * p + 1];
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-              const f32x16 &ga = acc[i][2 * p], &ua = acc[i][2 * p + 1];
-              *reinterpret_cast<uint2 *>(gr + 8 * gq + 4 * h) =
-                  make_uint2(pack2(ga[4 * gq], ga[4 * gq + 1]), pack2(ga[4 * gq + 2], ga[4 * gq + 3]));
-              *reinterpret_cast<uint2 *>(gr + 32 + 8 * gq + 4 * h) =
-                  make_uint2(pack2(ua[4 * gq], ua[4 * gq + 1]), pack2(ua[4 * gq + 2], ua[4 * gq + 3]));
+            for (int q = 0; q < 2; ++q) {
+              uint32_t g0 = pack2(ga[8 * q], ga[8 * q + 1]), g1 = pack2(ga[8 * q + 2], ga[8 * q + 3]);
+              uint32_t g2 = pack2(ga[8 * q + 4], ga[8 * q + 5]), g3 = pack2(ga[8 * q + 6], ga[8 * q + 7]);
+              uint32_t u0 = pack2(ua[8 * q], ua[8 * q + 1]), u1 = pack2(ua[8 * q + 2], ua[8 * q + 3]);
+              uint32_t u2 = pack2(ua[8 * q + 4], ua[8 * q + 5]), u3 = pack2(ua[8 * q + 6], ua[8 * q + 7]);
+              swap_halves(g0, g2);
+              swap_halves(g1, g3);
+              swap_halves(u0, u2);
+              swap_halves(u1, u3);
+              if (row_ok) {
+                *reinterpret_cast<uint4 *>(gr + 16 * q + 8 * h) = make_uint4(g0, g1, g2, g3);
+                *reinterpret_cast<uint4 *>(gr + 32 + 16 * q + 8 * h) = make_uint4(u0, u1, u2, u3);
+              }
             }
           }
         }
@@ -760,14 +780,26 @@ void gemm256_kernel(GemmArgs g) {
         const int col0 = c.n0 + wn * WN + j * 32;
         return (int64_t(pr >> 4) * gu_blocks + (col0 >> 5) * 2) * 512 + (pr & 15) * 32;
       };
+      // 16-byte loads (lane l: columns 16 q + 0..7, lane l + 32: 16 q + 8..15),
+      // then half-wave swaps give each lane its accumulator columns
+      // 8 gq + 4 h + 0..3
       auto load_block = [&](int i, int j, uint2 (&gw)[4], uint2 (&uw)[4]) {
         const bool ok = block_ok(i, j) && i * 32 + (lane & 31) < rows_w;
         const int64_t gb = ok ? gu_index(i, j) : 0;
 #pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-          const int cc = 8 * gq + 4 * h;
-          gw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + cc) : make_uint2(0u, 0u);
-          uw[gq] = ok ? *reinterpret_cast<const uint2 *>(g.GU + gb + 32 + cc) : make_uint2(0u, 0u);
+        for (int q = 0; q < 2; ++q) {
+          const int cc = 16 * q + 8 * h;
+          uint4 x = ok ? *reinterpret_cast<const uint4 *>(g.GU + gb + cc) : make_uint4(0u, 0u, 0u, 0u);
+          uint4 y = ok ? *reinterpret_cast<const uint4 *>(g.GU + gb + 32 + cc)
+                       : make_uint4(0u, 0u, 0u, 0u);
+          swap_halves(x.x, x.z);
+          swap_halves(x.y, x.w);
+          swap_halves(y.x, y.z);
+          swap_halves(y.y, y.w);
+          gw[2 * q] = make_uint2(x.x, x.y);
+          gw[2 * q + 1] = make_uint2(x.z, x.w);
+          uw[2 * q] = make_uint2(y.x, y.y);
+          uw[2 * q + 1] = make_uint2(y.z, y.w);
         }
       };
       uint2 gcur[4], ucur[4], gnxt[4], unxt[4];
@@ -782,37 +814,54 @@ void gemm256_kernel(GemmArgs g) {
           const int64_t kb = (kb_grp + rr) >> 5;
           const int col0 = c.n0 + wn * WN + j * 32;  // first activation column f
           const int64_t gblk = dgu_index(i, j);
+          // two column groups gq = 2 q, 2 q + 1 at a time (columns
+          // 8 gq + 4 h + e of the 32-block; rows past the group's end 0)
+          uint16_t *dgu = g.C;
 #pragma unroll
-          for (int gq = 0; gq < 4; ++gq) {
-            const int cc = 8 * gq + 4 * h;  // column inside the 32-block
-            float dg[4] = {0.f, 0.f, 0.f, 0.f}, du[4] = {0.f, 0.f, 0.f, 0.f},
-                  av[4] = {0.f, 0.f, 0.f, 0.f};
-            if (row_ok) {
-              const uint2 gw = gcur[gq], uw = ucur[gq];
+          for (int q = 0; q < 2; ++q) {
+            float dg[2][4], du[2][4], av[2][4];
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+              const uint2 gw = gcur[2 * q + s], uw = ucur[2 * q + s];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                const uint32_t gbits = (e < 2 ? gw.x : gw.y) >> (16 * (e & 1));
-                const uint32_t ubits = (e < 2 ? uw.x : uw.y) >> (16 * (e & 1));
-                const float gv = __uint_as_float(gbits << 16), uv = __uint_as_float(ubits << 16);
-                const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-gv));
-                const float da = acc[i][j][4 * gq + e];
-                dg[e] = da * uv * (sg * (1.0f + gv * (1.0f - sg)));
-                du[e] = da * (gv * sg);
-                av[e] = gv * sg * uv;
+                dg[s][e] = du[s][e] = av[s][e] = 0.0f;
+                if (row_ok) {
+                  const uint32_t gbits = (e < 2 ? gw.x : gw.y) >> (16 * (e & 1));
+                  const uint32_t ubits = (e < 2 ? uw.x : uw.y) >> (16 * (e & 1));
+                  const float gv = __uint_as_float(gbits << 16), uv = __uint_as_float(ubits << 16);
+                  const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-gv));
+                  const float da = acc[i][j][4 * (2 * q + s) + e];
+                  dg[s][e] = da * uv * (sg * (1.0f + gv * (1.0f - sg)));
+                  du[s][e] = da * (gv * sg);
+                  av[s][e] = gv * sg * uv;
+                }
               }
-              uint16_t *dgu = g.C;
-              *reinterpret_cast<uint2 *>(dgu + gblk + cc) =
-                  make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
-              *reinterpret_cast<uint2 *>(dgu + gblk + 512 + cc) =
-                  make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));
             }
             // transposed staging: output o at o * 1024 elements, [column][row]
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int n = (cc + e) * 32 + (lane & 31);
-              st16[n] = f32_to_bf16(dg[e]);
-              st16[1024 + n] = f32_to_bf16(du[e]);
-              st16[2048 + n] = f32_to_bf16(av[e]);
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int n = (8 * (2 * q + s) + 4 * h + e) * 32 + (lane & 31);
+                st16[n] = f32_to_bf16(dg[s][e]);
+                st16[1024 + n] = f32_to_bf16(du[s][e]);
+                st16[2048 + n] = f32_to_bf16(av[s][e]);
+              }
+            // [d g | d u] blocked, as 16-byte runs after the half-wave swaps
+            // (lane l: columns 16 q + 0..7, lane l + 32: 16 q + 8..15)
+            uint32_t a0 = pack2(dg[0][0], dg[0][1]), a1 = pack2(dg[0][2], dg[0][3]);
+            uint32_t a2 = pack2(dg[1][0], dg[1][1]), a3 = pack2(dg[1][2], dg[1][3]);
+            uint32_t b0 = pack2(du[0][0], du[0][1]), b1 = pack2(du[0][2], du[0][3]);
+            uint32_t b2 = pack2(du[1][0], du[1][1]), b3 = pack2(du[1][2], du[1][3]);
+            swap_halves(a0, a2);
+            swap_halves(a1, a3);
+            swap_halves(b0, b2);
+            swap_halves(b1, b3);
+            if (row_ok) {
+              *reinterpret_cast<uint4 *>(dgu + gblk + 16 * q + 8 * h) = make_uint4(a0, a1, a2, a3);
+              *reinterpret_cast<uint4 *>(dgu + gblk + 512 + 16 * q + 8 * h) =
+                  make_uint4(b0, b1, b2, b3);
             }
           }
           // d gate rows 64 (f / 32) + 0..31 and d up rows + 32 of [2F][kmax];
