@@ -295,7 +295,9 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
  * give undefined gradients. Null gate_up: g and u are recomputed (one more
  * grouped GEMM, into the workspace). Workspace of at least
  * llep_grouped_ffn_backward_workspace_bytes bytes, 256-byte aligned.
- * Requires D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned.
+ * Requires D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned; T*K below about
+ * 4.19 M pairs (the weight-gradient operands, each expert's rows end to end,
+ * are addressed with 32-bit byte offsets; LLEP_E_ARG beyond).
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */
 size_t llep_grouped_ffn_backward_workspace_bytes(const llep_plan_params *params,
                                                  int32_t D, int32_t F,

@@ -322,6 +322,8 @@ int llep_grouped_ffn_backward(const llep_plan_params *params, const llep_plan_bu
       !aligned16(w_gate_up_t_packed) || !aligned16(w_down_t_packed) || !aligned16(dx_perm) ||
       !aligned16(dw_gate) || !aligned16(dw_up) || !aligned16(dw_down) || !aligned16(gate_up))
     return fail(LLEP_E_ARG, "data not 16-byte aligned");
+  if (!llep::ffn_backward_rows_ok(params->T * params->K, params->E, params->P))
+    return fail(LLEP_E_ARG, "T * K too large for the backward (about 4 M pairs at most)");
   const size_t need =
       llep::ffn_backward_workspace_bytes(params->T * params->K, params->E, params->P, D, F, dtype);
   if (!workspace || workspace_bytes < need)

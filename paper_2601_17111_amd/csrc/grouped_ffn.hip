@@ -22,6 +22,8 @@
 // matrix, gate columns 32j..32j+31 are followed by the matching up columns,
 // so one wave holds gate and up values of the same output element in the
 // same accumulator register slot and applies SwiGLU without data exchange.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -212,19 +214,28 @@ constexpr int kStages = kAhead + 1;
 // pending LDS write: it would otherwise wait for every DMA in flight before
 // each LDS read. The kernel orders DMA and reads itself (wait_cnt + barrier);
 // DMA completions are in issue order, so the compiler's own vmcnt waits for
-// other loads stay correct (they can only wait longer).
-__device__ __forceinline__ void dma16(const void *src, uint32_t lds) {
+// other loads stay correct (they can only wait longer). The global address
+// is a wave-uniform 64-bit base in SGPRs plus a per-lane 32-bit byte offset
+// (the instruction's saddr form), so no lane computes a 64-bit address; the
+// LDS destination (1 KB, 16 bytes per lane) starts at m0.
+__device__ __forceinline__ void dma16(const char *base_in, int32_t voff, uint32_t lds) {
+  // the base is wave-uniform by construction; readfirstlane states it (the
+  // builtin returns int: both halves are widened as unsigned)
+  const uint64_t bv = reinterpret_cast<uint64_t>(base_in);
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(bv)));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(bv >> 32)));
+  const uint64_t base = (uint64_t(hi) << 32) | uint64_t(lo);
   // m0 is reserved to the compiler: saved and restored inside the asm
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
       "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
       "s_nop 0\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "s"(lds), "v"(src)
+      : "s"(lds), "v"(voff), "s"(base)
       : "memory");
 }
 
@@ -449,12 +460,12 @@ void gemm256_kernel(GemmArgs g) {
     const int kbb = kt * 1024;
 #pragma unroll
     for (int j = 0; j < A_PER_WAVE; ++j)
-      if (wave < NWD) dma16(Ab + offA[j] + kba, a_st + (wave + NWD * j) * 1024);
+      if (wave < NWD) dma16(Ab + kba, offA[j], a_st + (wave + NWD * j) * 1024);
 #pragma unroll
     for (int j = 0; j < B_FULL; ++j)
-      if (wave < NWD) dma16(Bb + offB[j] + kbb, b_st + (wave + NWD * j) * 1024);
+      if (wave < NWD) dma16(Bb + kbb, offB[j], b_st + (wave + NWD * j) * 1024);
     if (B_REM != 0 && wave < B_REM)
-      dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NWD * B_FULL) * 1024);
+      dma16(Bb + kbb, offB[B_SLOTS - 1], b_st + (wave + NWD * B_FULL) * 1024);
   };
   auto prologue = [&]() {
 #pragma unroll
@@ -496,8 +507,11 @@ void gemm256_kernel(GemmArgs g) {
   // The scheduling barriers keep that order, so the memory instructions issue
   // while the MFMAs execute instead of in bursts between them.
   constexpr int NM = TM * TN, NR = TM + TN, ND = A_PER_WAVE + B_SLOTS;
-  auto side_op = [&](int q, int st_next, int ks_next, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN],
-                     int st_dma, int kt_dma) {
+  // dma_wave: std::true_type for the waves that issue the DMA, else
+  // std::false_type (their DMA side operations are empty)
+  auto side_op = [&](auto dma_wave, int q, int st_next, int ks_next, bf16x8 (&fa)[TM],
+                     bf16x8 (&fb)[TN], int st_dma, int kt_dma) {
+    constexpr bool kDmaWave = decltype(dma_wave)::value;
     if (q < TM) {
       const uint16_t *a_s = stageA(st_next);
       fa[q] = *reinterpret_cast<const bf16x8 *>(
@@ -506,21 +520,20 @@ void gemm256_kernel(GemmArgs g) {
       const uint16_t *b_s = stageB(st_next);
       fb[q - TM] = *reinterpret_cast<const bf16x8 *>(
           &b_s[lds_swz32(wn * WN + (q - TM) * 32 + (lane & 31), ks_next * 2 + (lane >> 5))]);
-    } else {
+    } else if constexpr (kDmaWave) {
       const int d = q - NR;
       const uint32_t a_st = sA0 + st_dma * STAGE_BYTES, b_st = sB0 + st_dma * STAGE_BYTES;
       const int kba = kABlocked ? kt_dma * 1024 : kt_dma * kSK * 2;
       const int kbb = kt_dma * 1024;
-      if (wave >= NWD) return;
       if (d < A_PER_WAVE)
-        dma16(Ab + offA[d] + kba, a_st + (wave + NWD * d) * 1024);
+        dma16(Ab + kba, offA[d], a_st + (wave + NWD * d) * 1024);
       else if (d < A_PER_WAVE + B_FULL)
-        dma16(Bb + offB[d - A_PER_WAVE] + kbb, b_st + (wave + NWD * (d - A_PER_WAVE)) * 1024);
+        dma16(Bb + kbb, offB[d - A_PER_WAVE], b_st + (wave + NWD * (d - A_PER_WAVE)) * 1024);
       else if (wave < B_REM)
-        dma16(Bb + offB[B_SLOTS - 1] + kbb, b_st + (wave + NWD * B_FULL) * 1024);
+        dma16(Bb + kbb, offB[B_SLOTS - 1], b_st + (wave + NWD * B_FULL) * 1024);
     }
   };
-  auto interleaved_step = [&](f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM],
+  auto interleaved_step = [&](auto dma_wave, f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM],
                               const bf16x8 (&fb)[TN], bf16x8 (&fa_next)[TM],
                               bf16x8 (&fb_next)[TN], int st_next, int ks_next, bool with_dma,
                               int st_dma, int kt_dma) {
@@ -533,7 +546,7 @@ void gemm256_kernel(GemmArgs g) {
 #pragma unroll
       for (int q = 0; q < NR + ND; ++q) {
         if (q < NS && q * NM >= s * NS && q * NM < (s + 1) * NS) {
-          side_op(q, st_next, ks_next, fa_next, fb_next, st_dma, kt_dma);
+          side_op(dma_wave, q, st_next, ks_next, fa_next, fb_next, st_dma, kt_dma);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -577,16 +590,24 @@ void gemm256_kernel(GemmArgs g) {
       // past slice kt + 1 (compile-time wait count). The last slice is peeled
       // so no branch joins around the LDS reads (the wait inserted at such a
       // join would drain the fresh reads).
-      for (; kt < nk - kAhead; ++kt) {
-        // k-step 0 of slice kt; reads of its k-step 1; DMA of slice kt + kAhead
-        interleaved_step(acc, fa0, fb0, fa1, fb1, st, 1, true, st_req, kt_req);
-        st_req = next_stage(st_req);
-        ++kt_req;
-        wait_and_sync<(kAhead - 1) * PER_STAGE>();
-        st = next_stage(st);
-        // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1
-        interleaved_step(acc, fa1, fb1, fa0, fb0, st, 0, false, 0, 0);
-      }
+      // (one copy of the loop for the DMA-issuing waves and one for the
+      // others, so the DMA needs no per-instruction branch)
+      auto steady = [&](auto dma_wave) {
+        for (; kt < nk - kAhead; ++kt) {
+          // k-step 0 of slice kt; reads of its k-step 1; DMA of slice kt + kAhead
+          interleaved_step(dma_wave, acc, fa0, fb0, fa1, fb1, st, 1, true, st_req, kt_req);
+          st_req = next_stage(st_req);
+          ++kt_req;
+          wait_and_sync<(kAhead - 1) * PER_STAGE>();
+          st = next_stage(st);
+          // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1
+          interleaved_step(dma_wave, acc, fa1, fb1, fa0, fb0, st, 0, false, 0, 0);
+        }
+      };
+      if (wave < NWD)
+        steady(std::true_type{});
+      else
+        steady(std::false_type{});
       // tail: everything is requested; nk - 2 - kt slices remain past kt + 1
       for (; kt < nk - 1; ++kt) {
         read_frags(st, 1, fa1, fb1);
@@ -1234,6 +1255,11 @@ static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t 
 // [Wg | Wu]) and the activation, per x_perm row
 static size_t f32_bwd_bytes(int64_t R, int32_t F) {
   return 256 + round256(size_t(R) * 3 * F * 4);
+}
+
+bool ffn_backward_rows_ok(int64_t R, int32_t E, int32_t P) {
+  // a DMA lane's byte offset reaches 16 blocks of kmax / 32 KB each
+  return bwd_layout(R, E, P, 64, 64).kmax * 512 <= int64_t(INT32_MAX);
 }
 
 size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F,

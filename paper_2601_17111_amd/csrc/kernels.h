@@ -90,6 +90,9 @@ struct FfnBwdArgs {
 };
 size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, int32_t F,
                                     llep_dtype dtype);
+// false when the weight-gradient operands of R rows are too long for the
+// GEMM's 32-bit per-lane byte offsets
+bool ffn_backward_rows_ok(int64_t R, int32_t E, int32_t P);
 hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream);
 hipError_t launch_pack_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype, const void *w_gate,
                                 const void *w_up, const void *w_down, void *gut, void *dnt,

@@ -203,6 +203,12 @@ def test_backward_argument_checks():
     assert call(**dict(ok, nbytes=need - 1)) == B.LLEP_E_WORKSPACE
     assert call(**dict(ok, ws=ctypes.c_void_p((1 << 24) + 64))) == B.LLEP_E_WORKSPACE
     assert call(**dict(ok, gate_up=ctypes.c_void_p(4104))) == B.LLEP_E_ARG
+    # more pairs than the backward's 32-bit operand offsets reach
+    big = B.make_params(1 << 20, 8, 8, 4, (1 << 23) // 4)
+    nb = B.llep_grouped_ffn_backward_workspace_bytes(big, 64, 128, bf)
+    assert L.llep_grouped_ffn_backward(ctypes.byref(big), ctypes.byref(bufs), 0, a, a, a, a, a,
+                                       None, 64, 128, bf, a, a, a, a, ws, nb, None) == B.LLEP_E_ARG
+    assert "too large" in B.last_error()
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
