@@ -454,3 +454,39 @@ def test_backward_from_saved_gate_up_is_bit_identical(dev, dtype):
         got_d = run.backward(d, save=True, fwd_device=fwd)
         for a, b in zip(got_d[2:], ref_d[2:]):
             assert np.array_equal(a, b), fwd
+
+
+@pytest.mark.parametrize("E,P,alpha", [(512, 64, (1, 1)), (512, 8, (11, 10)), (256, 64, (5, 4))])
+def test_layer_max_experts_and_devices(dev, E, P, alpha):
+    """The largest expert and device counts the library takes (512 experts,
+    64 devices), zipf routing with many spills: the layer output, the input
+    and gate gradients and every expert's weight gradients against the
+    oracle's plan-free values, and every device's partials summed in return
+    order give the totals."""
+    import torch
+    cfg = _cfg("max", alpha=alpha, routing=("zipf", 1.2), T=1500, D=64, F=64, E=E, K=8, P=P)
+    run = BwdRun(cfg, 12, dev)
+    y = run.forward(-1).float().cpu().numpy()
+    W = run.host_weights(range(E))
+    x = run.x.float().cpu().numpy()
+    want_y = oracle.moe_output(x, run.inp.ids, run.inp.gates, lambda e: W[e])
+    assert rel_err(y, want_y) <= TOL_BF16
+    dx, dgates, dwg, dwu, dwd = run.backward(-1, save=True)
+    assert run.layer.bufs.info_dict()["n_xfers"] > 0
+    want_dx, want_dg, want_dW = oracle.moe_backward(x, run.inp.ids, run.inp.gates,
+                                                    lambda e: W[e], run.dy.float().cpu().numpy(),
+                                                    E)
+    assert rel_err(dx, want_dx) <= TOL_BF16
+    assert rel_err(dgates, want_dg) <= TOL_BF16
+    for e in range(E):
+        if e not in want_dW:
+            assert not dwg[e].any() and not dwd[e].any()
+            continue
+        for got, want in zip((dwg[e], dwu[e], dwd[e]), want_dW[e]):
+            assert rel_err(got, want) <= TOL_BF16, e
+    acc = [np.zeros_like(t) for t in (dwg, dwu, dwd)]
+    for d in range(P):
+        for a, p in zip(acc, run.backward(d)[2:]):
+            a += p
+    for a, t in zip(acc, (dwg, dwu, dwd)):
+        assert rel_err(a, t) <= 1e-5
