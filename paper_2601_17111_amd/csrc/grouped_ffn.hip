@@ -700,7 +700,9 @@ void gemm256_kernel(GemmArgs g) {
               const float gv = acc[i][2 * p][4 * gq + e], uv = acc[i][2 * p + 1][4 * gq + e];
               hv[e] = gv * __builtin_amdgcn_rcpf(1.0f + __expf(-gv)) * uv;
             }
-            *reinterpret_cast<uint2 *>(blk + (8 * gq + 4 * h) * 2) =
+            // 16-byte chunk gq of the row, XOR-swizzled by (row / 4) % 4 so
+            // the 16 rows of a block spread over the banks
+            *reinterpret_cast<uint2 *>(blk + ((gq ^ ((lane >> 2) & 3)) << 4) + 8 * h) =
                 make_uint2(pack2(hv[0], hv[1]), pack2(hv[2], hv[3]));
           }
         }
@@ -738,34 +740,8 @@ void gemm256_kernel(GemmArgs g) {
         for (int rb = 0; rb < WM / 16; ++rb) {
           if (rb * 16 >= rows_w) break;  // the group's padded rows end here
           *reinterpret_cast<i32x4 *>(dst + int64_t(rb) * (g.ldc >> 5) * 1024) =
-              *reinterpret_cast<const i32x4 *>(sp + rb * 1024 + lane * 16);
-        }
-      }
-    } else if constexpr (kEpi == kEpiPlain && kCBlocked) {
-      // blocked C over padded rows: per 32-column block, one 1 KB block per
-      // 16 rows of the wave's part
-      static_assert((WM / 16) * 1024 <= STAGING, "staging");
-      const int64_t rb0 = (c.prow0 + c.m0 + wm * WM) >> 4;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col0 = c.n0 + wn * WN + j * 32;
-        if (col0 >= g.N) continue;
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          char *blk = stg + (2 * i + ((lane & 31) >> 4)) * 1024 + (lane & 15) * 64;
-#pragma unroll
-          for (int gq = 0; gq < 4; ++gq)
-            *reinterpret_cast<uint2 *>(blk + (8 * gq + 4 * h) * 2) =
-                make_uint2(pack2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
-                           pack2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]));
-        }
-        char *dst = reinterpret_cast<char *>(g.C) + (rb0 * (g.ldc >> 5) + (col0 >> 5)) * 1024 +
-                    lane * 16;
-#pragma unroll
-        for (int rb = 0; rb < WM / 16; ++rb) {
-          if (rb * 16 >= rows_w) break;
-          *reinterpret_cast<i32x4 *>(dst + int64_t(rb) * (g.ldc >> 5) * 1024) =
-              *reinterpret_cast<const i32x4 *>(stg + rb * 1024 + lane * 16);
+              *reinterpret_cast<const i32x4 *>(
+              sp + rb * 1024 + (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) << 4));
         }
       }
     } else if constexpr (kEpi == kEpiSwigluBwd) {
@@ -949,7 +925,9 @@ void gemm256_kernel(GemmArgs g) {
       // row-major C: 32 rows x WN columns per piece, rows RS bytes apart
       auto rowmajor_epilogue = [&]() {
         static_assert(!kCBlocked, "blocked C: other epilogues");
-        constexpr int RS = WN * 2;
+        // row stride padded by 16 bytes: the 32 rows of a piece then fall
+        // into different banks
+        constexpr int RS = WN * 2 + 16;
         constexpr int CH = WN / 8;  // 16-byte chunks per row segment
         static_assert(32 * RS <= STAGING, "staging");
         const int ncol0 = c.n0 + wn * WN;
