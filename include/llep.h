@@ -86,6 +86,7 @@ extern "C" {
 /* ---- limits --------------------------------------------------------------- */
 #define LLEP_MAX_EXPERTS 512
 #define LLEP_MAX_DEVICES 64
+#define LLEP_MAX_FFN_DIM 65536 /* largest D and F of the FFN entry points */
 
 typedef enum { LLEP_F32 = 0, LLEP_BF16 = 1 } llep_dtype;
 typedef enum { LLEP_MODE_LLEP = 0, LLEP_MODE_EP = 1 } llep_mode;
@@ -179,7 +180,7 @@ int llep_permute(const llep_plan_params *params, const llep_plan_buffers *plan,
  *                               of w_gate, P row 64j + 32 + c = column
  *                               32j + c of w_up (j < F/32, c < 32);
  *   w_down_packed    [E][D*F]:  K = F; P row d = column d of w_down.
- * Requires D % 64 == 0 and F % 64 == 0.
+ * Requires D % 64 == 0 and F % 64 == 0, both at most LLEP_MAX_FFN_DIM.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
 size_t llep_packed_gate_up_bytes(int32_t E, int32_t D, int32_t F,
                                  llep_dtype dtype);
@@ -197,7 +198,8 @@ int llep_pack_weights(int32_t E, int32_t D, int32_t F, llep_dtype dtype,
  * The group range is read from plan->group_begin on the device: no host
  * synchronization. Weights are the llep_pack_weights outputs. bf16 uses
  * matrix cores (MFMA); f32 is a plain reference-precision path.
- * Requires D % 64 == 0, F % 64 == 0; workspace of at least
+ * Requires D % 64 == 0, F % 64 == 0 (both at most LLEP_MAX_FFN_DIM);
+ * workspace of at least
  * llep_grouped_ffn_workspace_bytes(params, F, dtype) bytes, 256-byte aligned.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */
 size_t llep_grouped_ffn_workspace_bytes(const llep_plan_params *params,
@@ -264,7 +266,7 @@ int llep_combine_backward(const llep_plan_params *params, const void *out_perm,
  *                                 w_up[d][32j + c] (the forward's gate/up
  *                                 interleave along the contraction);
  *   w_down_t_packed    [E][F*D]:  K = D; P row f = row f of w_down.
- * Requires D % 64 == 0, F % 64 == 0.
+ * Requires D % 64 == 0, F % 64 == 0, both at most LLEP_MAX_FFN_DIM.
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE. */
 int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype,
                                const void *w_gate, const void *w_up,
@@ -295,7 +297,8 @@ int llep_pack_weights_backward(int32_t E, int32_t D, int32_t F, llep_dtype dtype
  * give undefined gradients. Null gate_up: g and u are recomputed (one more
  * grouped GEMM, into the workspace). Workspace of at least
  * llep_grouped_ffn_backward_workspace_bytes bytes, 256-byte aligned.
- * Requires D % 64 == 0, F % 64 == 0; dw_* 16-byte aligned; T*K below about
+ * Requires D % 64 == 0, F % 64 == 0 (at most LLEP_MAX_FFN_DIM); dw_*
+ * 16-byte aligned; T*K below about
  * 4.19 M pairs (the weight-gradient operands, each expert's rows end to end,
  * are addressed with 32-bit byte offsets; LLEP_E_ARG beyond).
  * Errors: LLEP_E_ARG, LLEP_E_DTYPE, LLEP_E_WORKSPACE. */

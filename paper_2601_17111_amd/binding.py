@@ -27,6 +27,7 @@ LLEP_MODE_EP = 1
 LLEP_STATUS_BAD_EXPERT_ID = 1
 LLEP_MAX_EXPERTS = 512
 LLEP_MAX_DEVICES = 64
+LLEP_MAX_FFN_DIM = 65536
 
 EXPORTED = [
     "llep_plan", "llep_permute", "llep_grouped_ffn", "llep_combine",

@@ -66,6 +66,9 @@ int check_ffn_dims(int32_t D, int32_t F, llep_dtype dtype) {
   if (elem_bytes(dtype) == 0) return fail(LLEP_E_DTYPE, "unknown dtype");
   if (D < 64 || D % 64 != 0) return fail(LLEP_E_ARG, "D must be a positive multiple of 64");
   if (F < 64 || F % 64 != 0) return fail(LLEP_E_ARG, "F must be a positive multiple of 64");
+  // the GEMMs address a tile's operand rows with 32-bit byte offsets
+  if (D > LLEP_MAX_FFN_DIM || F > LLEP_MAX_FFN_DIM)
+    return fail(LLEP_E_ARG, "D and F must be at most LLEP_MAX_FFN_DIM");
   return LLEP_OK;
 }
 

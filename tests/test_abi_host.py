@@ -141,6 +141,8 @@ def test_ffn_argument_checks():
                                   dtype, a, ws, nbytes, None)
     assert call(**ok_args(D=96)) == B.LLEP_E_ARG          # D % 64
     assert call(**ok_args(F=100)) == B.LLEP_E_ARG         # F % 64
+    assert call(**ok_args(D=B.LLEP_MAX_FFN_DIM + 64)) == B.LLEP_E_ARG
+    assert call(**ok_args(F=B.LLEP_MAX_FFN_DIM + 64)) == B.LLEP_E_ARG
     assert call(**ok_args(device=4)) == B.LLEP_E_ARG      # device >= P
     assert call(**ok_args(device=-2)) == B.LLEP_E_ARG
     assert call(**ok_args(dtype=3)) == B.LLEP_E_DTYPE
