@@ -173,7 +173,9 @@ def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps):
     layer.backward(dy, run["gates"], run["gu"], gut, dnt, dstar)  # allocates the buffers
     L = layer
 
-    def step(gate_up):
+    def step(gate_up, e):
+        """One backward step; e[0..3] are recorded around its three calls."""
+        e[0].record()
         B.llep_combine_backward(L.params, L.out_perm, L.pair_row, run["gates"], dy, L.d_out_perm,
                                 L.d_gates)
         e[1].record()
@@ -182,22 +184,19 @@ def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps):
                                     L.bwd_workspace, gate_up=gate_up)
         e[2].record()
         B.llep_combine(L.params, L.dx_perm, L.pair_row, None, L.dx)
+        e[3].record()
 
     def timed(gate_up):
-        nonlocal e
         seg = {"combine_backward": 0.0, "grouped_ffn_backward": 0.0, "dx_sum": 0.0}
         for i in range(steps + 2):
             e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-            e[0].record()
-            step(gate_up)
-            e[3].record()
+            step(gate_up, e)
             torch.cuda.synchronize()
             if i >= 2:
                 for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
                     seg[k] += a.elapsed_time(b) / steps
         return seg
 
-    e = None
     seg = timed(L.gate_up)
     recompute_ms = timed(None)["grouped_ffn_backward"]
     # the training forward's grouped FFN on d*: the inference one plus the
