@@ -1258,7 +1258,7 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase,
     int32_t *__restrict__ chunk_group, int4 *__restrict__ wg_experts, int32_t *__restrict__ n_wg,
     int32_t *__restrict__ kslices, int32_t *__restrict__ queue) {
-  __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks];
+  __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks], skb[kMaxChunks];
   __shared__ int32_t esl[LLEP_MAX_EXPERTS];
   const int tid = threadIdx.x;
   const int lo = device < 0 ? group_begin[0] : group_begin[device];
@@ -1277,7 +1277,7 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     for (int j = 0; j < G; ++j)
       if (se[j] < se[i] || (se[j] == se[i] && skey[j] < skey[i])) kb += ssl[j];
     kbase[lo + i] = kb * 32;
-    for (int c = kb; c < kb + ssl[i]; ++c) chunk_group[c] = lo + i;
+    skb[i] = kb;
   }
   for (int e = tid; e < E; e += blockDim.x) {
     int32_t sl = 0;
@@ -1285,6 +1285,9 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     esl[e] = sl;
   }
   __syncthreads();
+  // owner group of every 32-row slice, all threads striding over each group
+  for (int i = 0; i < G; ++i)
+    for (int c = skb[i] + tid; c < skb[i] + ssl[i]; c += blockDim.x) chunk_group[c] = lo + i;
   for (int e = tid; e < E; e += blockDim.x) {
     const int32_t sl = esl[e];
     if (sl == 0) continue;
