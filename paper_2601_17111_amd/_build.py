@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libllep.so")
 
-SOURCES = ["plan.hip", "permute.hip", "grouped_ffn.hip", "abi.cpp"]
+SOURCES = ["plan.hip", "permute.hip", "grouped_ffn.hip", "grouped_ffn_bwd.hip", "abi.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
