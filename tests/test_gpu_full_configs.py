@@ -111,16 +111,17 @@ def _expert_subset(cfg, ids, n_extra, rng):
     return sorted(set(hot + rest))
 
 
-FFN_CASES = ["gpt-oss-20b", "gpt-oss-120b-hot16", "gpt-oss-120b-hot4", "gpt-oss-120b-hot1",
-             "qwen3-30b-a3b", "deepseek-v3"]
+FFN_CASES = [(n, 0) for n in ("gpt-oss-20b", "gpt-oss-120b-hot16", "gpt-oss-120b-hot4",
+                               "gpt-oss-120b-hot1", "qwen3-30b-a3b", "deepseek-v3")]
+FFN_CASES += [("gpt-oss-120b-hot1", 1), ("qwen3-30b-a3b", 2)]
 
 
-@pytest.mark.parametrize("name", FFN_CASES)
-def test_full_layer_outputs(dev, name):
+@pytest.mark.parametrize("name,seed", FFN_CASES, ids=lambda v: str(v))
+def test_full_layer_outputs(dev, name, seed):
     import torch
     cfg = _cfg(name)
-    run = LayerRun(cfg, 0, dev)
-    rng = np.random.default_rng(7)
+    run = LayerRun(cfg, seed, dev)
+    rng = np.random.default_rng(7 + seed)
     y = run.forward(-1).float().cpu().numpy()
     L = run.layer
     ids = run.inp.ids
