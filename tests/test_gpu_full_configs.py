@@ -186,7 +186,7 @@ def test_full_ep_equals_llep_bitwise(dev):
     assert torch.equal(y_llep, y_ep)
 
 
-BWD_CASES = ["gpt-oss-120b-hot1", "qwen3-30b-a3b", "deepseek-v3"]
+BWD_CASES = ["gpt-oss-20b", "gpt-oss-120b-hot1", "qwen3-30b-a3b", "deepseek-v3"]
 
 
 @pytest.mark.parametrize("name", BWD_CASES)
@@ -272,6 +272,24 @@ def test_full_backward(dev, name):
     for a, b in zip(saved, (dx, dg, dwg, dwu, dwd)):
         assert torch.equal(a, b)
     del saved
+    # the saved g, u themselves: sampled rows of the sampled experts' groups
+    # against the float64 projections of their token rows
+    info = L.bufs.info_dict()
+    row_pair = L.row_pair[:info["total_rows"]].cpu().numpy()
+    col = 32 * (np.arange(2 * cfg.F) // 64) + np.arange(2 * cfg.F) % 32
+    is_gate = np.arange(2 * cfg.F) % 64 < 32
+    checked = 0
+    for (d, e, r0, n) in L.bufs.groups[:info["n_groups"]].cpu().tolist():
+        if e not in S:
+            continue
+        rows = np.unique(np.array([r0, r0 + n - 1, r0 + int(rng.integers(0, n))]))
+        got = L.gate_up[torch.from_numpy(rows).to(dev)].float().cpu().numpy()
+        wg, wu, _ = (w.astype(np.float64) for w in W[e])
+        xr = x[row_pair[rows] // cfg.K]
+        want = np.where(is_gate, (xr @ wg)[:, col], (xr @ wu)[:, col])
+        assert rel_err(got, want) <= TOL_BF16, (d, e)
+        checked += 1
+    assert checked > 0
     L.gate_up = None
     if name != "deepseek-v3":
         L.set_mode("ep")
