@@ -129,9 +129,11 @@ __global__ __launch_bounds__(256) void rank_kernel(
 // out_perm raise the combine from 0.62-0.65 to 0.73-0.79 of HBM peak;
 // non-temporal loads in the gather gain nothing and non-temporal stores of
 // x_perm lose 10-15%; a persistent gather that requests the next token's row
-// before storing the current one measured no faster (the gather moves its
-// bytes at 5.9 TB/s, four fifths of them writes; a plain fill reaches 6.8). Four pairs' rows of at most 4 vectors per lane are in
-// flight per combine step (1 or 2 measured within 2%).
+// before storing the current one measured no faster, and one wave per
+// destination row (sequential writes, each token read K times) was 15-40%
+// slower (the gather moves its bytes at 5.9 TB/s, four fifths of them
+// writes; a plain fill reaches 6.8). Four pairs' rows of at most 4 vectors
+// per lane are in flight per combine step (1 or 2 measured within 2%).
 constexpr bool kGatherNtLoad = false;
 constexpr bool kGatherNtStore = false;
 constexpr bool kCombineNtLoad = true;
