@@ -787,19 +787,26 @@ void gemm256_kernel(GemmArgs g) {
             }
           }
           // d gate rows 64 (f / 32) + 0..31 and d up rows + 32 of [2F][kmax];
-          // act rows f of [F][kmax]; 16 rows per 1 KB block
+          // act rows f of [F][kmax]; 16 rows per 1 KB block. Non-temporal
+          // stores: these blocks are read only by the next launch, and kept
+          // out of the L2 they leave the operands of this GEMM there (0.5-1.2%
+          // faster backward; the same for the blocked [d g | d u] above,
+          // which the dX GEMM reads soon after, was 1-3% slower).
           const int64_t ngate = 2 * col0;  // = 64 * (col0 / 32)
 #pragma unroll
           for (int bb = 0; bb < 2; ++bb) {
             const i32x4 vg = *reinterpret_cast<const i32x4 *>(stg + bb * 1024 + lane * 16);
             const i32x4 vu = *reinterpret_cast<const i32x4 *>(stg + 2048 + bb * 1024 + lane * 16);
             const i32x4 va = *reinterpret_cast<const i32x4 *>(stg + 4096 + bb * 1024 + lane * 16);
-            *reinterpret_cast<i32x4 *>(g.dgu_t + (((ngate >> 4) + bb) * kblocks + kb) * 512 +
-                                       lane * 8) = vg;
-            *reinterpret_cast<i32x4 *>(g.dgu_t + ((((ngate + 32) >> 4) + bb) * kblocks + kb) * 512 +
-                                       lane * 8) = vu;
-            *reinterpret_cast<i32x4 *>(g.act_t + (((col0 >> 4) + bb) * kblocks + kb) * 512 +
-                                       lane * 8) = va;
+            __builtin_nontemporal_store(
+                vg, reinterpret_cast<i32x4 *>(g.dgu_t + (((ngate >> 4) + bb) * kblocks + kb) * 512 +
+                                              lane * 8));
+            __builtin_nontemporal_store(
+                vu, reinterpret_cast<i32x4 *>(
+                        g.dgu_t + ((((ngate + 32) >> 4) + bb) * kblocks + kb) * 512 + lane * 8));
+            __builtin_nontemporal_store(
+                va, reinterpret_cast<i32x4 *>(g.act_t + (((col0 >> 4) + bb) * kblocks + kb) * 512 +
+                                              lane * 8));
           }
         }
         if (b + 1 < TM * TN) {
