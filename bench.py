@@ -117,15 +117,12 @@ def _traffic(workload):
 
 
 def _m_local_gb(layer, P, D, F, eb):
-    """Peak memory model of each device's share (Sec. 3 cost analysis):
-    sum over the device's groups of (n D + 3 D F + n F) elements, n its rows,
-    3 D F the SwiGLU expert's three weight matrices."""
+    """Peak memory model of each device's share (Sec. 3.2, Eq. 4, with the
+    SwiGLU expert's three weight matrices) from the plan's group table, GB."""
+    from paper_2601_17111_amd.layer import m_local_bytes
     info = layer.bufs.info_dict()
     groups = layer.bufs.groups[:info["n_groups"]].cpu().tolist()
-    out = [0.0] * P
-    for d, _, _, n in groups:
-        out[d] += (n * D + 3 * D * F + n * F) * eb / 1e9
-    return out
+    return [v / 1e9 for v in m_local_bytes(groups, P, D, F, eb)]
 
 
 def _time_steps(layer, run, steps, dstar):

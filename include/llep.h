@@ -14,15 +14,15 @@
  *   llep_plan         loads l, then the least-loaded plan (Alg. 2/3) or the
  *                     standard EP plan (Alg. 1), as device-resident tables
  *   llep_permute      gathers token rows into per-(device, expert, chunk)
- *                     order (Sec. 2.1 re-indexing; Alg. 4 sort, index_select,
- *                     build chunks)
+ *                     order (Sec. 2.1 re-indexing; Alg. 4 sorting, gathering,
+ *                     chunk building)
  *   llep_grouped_ffn  grouped SwiGLU expert GEMMs for one device's groups
  *                     (Alg. 4 grouped GEMMs over native and foreign experts;
  *                     three-matrix SwiGLU expert of Sec. 5.1);
  *                     llep_grouped_ffn_train also keeps g and u for the
  *                     backward
  *   llep_combine      gate-weighted sum of each token's K expert rows (Eq. 1;
- *                     Alg. 4 reverse_sort, reshape, sum over K)
+ *                     Alg. 4 un-sorting, reshape, sum over K)
  *
  * and the backward of steps 4 and 5 (LLEP stays exact under training; the
  * weight gradients of spilled chunks return to the expert's native device,
@@ -48,8 +48,8 @@
  *
  * Readings of the paper that bind these calls (the paper leaves them open):
  *   - capacity m_alpha (Alg. 2) is an integer count of pairs;
- *   - sort(l, decreasing) orders by load descending, expert id ascending;
- *     the devices of Alg. 3 order by g_a + g_p ascending, then index;
+ *   - Alg. 2's decreasing sort of the loads breaks ties by lower expert id;
+ *     Alg. 3 ranks devices by g_a + g_p ascending, then by index;
  *   - min_chunk < 1 is read as 1; Alg. 3 force-assigns to the least-loaded
  *     device other than the native one;
  *   - zero-load experts get no chunk; with P == 1 the plan is standard EP;

@@ -18,13 +18,14 @@ from .backward import (  # noqa: F401
     swiglu_ffn_backward,
 )
 from .llep import (  # noqa: F401
+    DeviceLedger,
     PlanResult,
     bypass_to_standard_ep,
     capacity_from_alpha,
     combine,
     expert_loads,
     least_loaded_assignment,
-    least_loaded_spill,
+    m_local,
     min_max_load_exhaustive,
     moe_output,
     pair_ranks,
@@ -32,6 +33,7 @@ from .llep import (  # noqa: F401
     plan,
     plan_tables,
     silu,
+    spill_to_least_loaded,
     standard_ep_assignment,
     swiglu_ffn,
 )

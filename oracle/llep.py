@@ -14,9 +14,10 @@ What is computed, and where the paper defines it:
                                      with the constraints paragraph of Sec. 4
 * the standard EP plan            -- Alg. 1 (experts [pM, (p+1)M-1] on device p)
 * the lambda bypass               -- Alg. 4, the max/mean imbalance test
-* the permutation                 -- Sec. 2.1 "Implementation" (re-indexing by
-                                     expert, token order kept inside an expert),
-                                     Alg. 4 sort / index_select / build chunks
+* the permutation                 -- Sec. 2.1, implementation paragraph
+                                     (re-indexing by expert, token order kept
+                                     inside an expert); Alg. 4's sorting,
+                                     gathering and chunk-building steps
 * the expert outputs              -- Eq. (1)-(2) with the three-matrix SwiGLU
                                      expert of Sec. 5.1; plan-free, float64
 
@@ -26,8 +27,8 @@ the GPU library):
 * capacity is an integer number of token-expert pairs; a real alpha is turned
   into one by ceil(alpha * sum(l) / P) with alpha as an exact rational;
 * sorting the loads (Alg. 2) orders by load descending, expert id ascending;
-* the "other GPUs sorted by g_a + g_p" of Alg. 3 order by that sum, then by
-  device index;
+* the other devices that Alg. 3 ranks by assigned plus pending load are
+  ranked by that sum, then by device index;
 * a minimum chunk size m below 1 is read as 1 (with m = 0 Alg. 3 could assign
   empty chunks forever);
 * the force-assign of Alg. 3 goes to the least-loaded *other* device (the
@@ -58,7 +59,7 @@ STATUS_BAD_EXPERT_ID = 1
 
 
 # ---------------------------------------------------------------------------
-# Step 1: expert loads (Alg. 4, "sum of loads of global experts")
+# Step 1: expert loads (Alg. 4, first step: the global per-expert loads)
 # ---------------------------------------------------------------------------
 
 def expert_loads(ids_flat: Sequence[int], E: int) -> Tuple[List[int], int]:
@@ -89,56 +90,94 @@ def capacity_from_alpha(total_load: int, alpha: Fraction, P: int) -> int:
 # Step 2: the plan (Alg. 2 LLA, Alg. 3 LLAS, Alg. 1 standard EP)
 # ---------------------------------------------------------------------------
 
-def least_loaded_spill(ng: int, r: int, to: int, A: List[Tuple[int, int, int]],
-                       g_a: List[int], g_p: List[int], cap: int, m: int,
-                       P: int) -> int:
-    """Alg. 3 (LLAS): spill r pairs of an expert native to device ng,
-    starting at pair offset `to`, onto the least-loaded other devices.
+class DeviceLedger:
+    """Per-device bookkeeping of the least-loaded assignment (Alg. 2).
 
-    Appends (device, start, end) to A and updates g_a in place. Returns the
-    number of force-assignments made.
+    placed[d]  -- pairs already given to device d (native or foreign);
+    pending[d] -- pairs of d's own experts that have not been visited yet,
+                  held in reserve so that a device keeps room for its own
+                  experts before it accepts foreign ones;
+    cap        -- the integer capacity m_alpha.
+
+    A device's occupancy is placed + pending; its free room is cap minus
+    that (negative once the device is over capacity).
     """
+
+    def __init__(self, native_load: List[int], cap: int):
+        self.placed = [0] * len(native_load)
+        self.pending = list(native_load)
+        self.cap = cap
+
+    def occupancy(self, d: int) -> int:
+        return self.placed[d] + self.pending[d]
+
+    def free(self, d: int) -> int:
+        return self.cap - self.occupancy(d)
+
+    def give(self, d: int, n: int) -> None:
+        self.placed[d] += n
+
+
+def spill_to_least_loaded(ledger: DeviceLedger, home: int, remaining: int,
+                          offset: int, m: int) -> Tuple[List[Tuple[int, int, int]], int]:
+    """The spill step (Alg. 3): place `remaining` pairs of an expert whose
+    native device is `home`, starting at pair offset `offset`, on the other
+    devices.
+
+    Each round ranks every other device by occupancy (ties: lower index) and
+    walks that ranking from the emptiest device on. A device is taken if the
+    piece it could hold -- its free room, at most the pairs still to place --
+    is at least m pairs, or is everything that is left. If no device
+    qualifies, all remaining pairs go to the emptiest other device even
+    though that exceeds its capacity (a force-assignment).
+
+    Returns the pieces (device, start, end) in the order they were made and
+    the number of force-assignments.
+    """
+    P = len(ledger.placed)
+    pieces: List[Tuple[int, int, int]] = []
     forced = 0
-    while r > 0:
-        # the other devices, least loaded first; ties keep device order
-        others = [g for g in range(P) if g != ng]
-        others.sort(key=lambda g: g_a[g] + g_p[g])  # stable sort
-        assigned = False
-        for o in others:
-            c = min(r, cap - g_a[o] - g_p[o])
-            if c < m and r > c:
-                continue  # chunk too small (and not the last one): skip o
-            A.append((o, to, to + c))
-            g_a[o] += c
-            r -= c
-            to += c
-            assigned = True
-            break
-        if not assigned:
-            # force-assign everything left to the least-loaded other device
-            o = others[0]
-            A.append((o, to, to + r))
-            g_a[o] += r
-            r = 0
+    while remaining > 0:
+        ranking = sorted((d for d in range(P) if d != home),
+                         key=lambda d: (ledger.occupancy(d), d))
+        target, take = None, 0
+        for d in ranking:
+            room = min(remaining, ledger.free(d))
+            if room >= m or room == remaining:
+                target, take = d, room
+                break
+        if target is None:
+            target, take = ranking[0], remaining
             forced += 1
-    return forced
+        pieces.append((target, offset, offset + take))
+        ledger.give(target, take)
+        offset += take
+        remaining -= take
+    return pieces, forced
 
 
 def least_loaded_assignment(loads: Sequence[int], M: int, cap: int, m: int
                             ) -> Tuple[Dict[int, List[Tuple[int, int, int]]],
                                        List[Tuple[int, int, int]], int]:
-    """Alg. 2 (LLA).
+    """The least-loaded assignment (Alg. 2).
 
     loads: per-expert load l (length N = P*M); M: experts per device;
     cap: integer capacity m_alpha; m: minimum pairs per spilled GEMM.
 
+    Experts are visited from the largest load to the smallest (ties: lower
+    expert id). Visiting an expert releases its reserved pairs from its
+    native device's pending load; the native device then keeps as many of
+    the expert's pairs as its free room allows (all of them, some, or none:
+    the three cases of Alg. 2), and the rest goes through the spill step.
+
     Returns (assignments, transfers, forced):
-      assignments[e] = [(device, start, end), ...] in the order Alg. 2/3 emit
-                       them (empty chunks dropped);
-      transfers      = sorted unique (expert, src, dst) weight moves (the
-                       weight-transfer plan W: every chunk of expert e on a
-                       device q != native(e) needs W_e moved native -> q);
-      forced         = number of Alg. 3 force-assignments.
+      assignments[e] = [(device, start, end), ...], non-empty pieces in the
+                       order they were made;
+      transfers      = sorted unique (expert, src, dst) weight moves: a piece
+                       of expert e on a device q other than its native one
+                       needs e's weights copied native -> q (the transfer
+                       plan W of Alg. 2);
+      forced         = number of force-assignments.
     """
     N = len(loads)
     assert N % M == 0
@@ -148,38 +187,25 @@ def least_loaded_assignment(loads: Sequence[int], M: int, cap: int, m: int
     if P == 1:
         # no other device to spill to: the plan is the standard EP plan
         return standard_ep_assignment(loads, M), [], 0
-    # sort(l, decreasing): load descending, expert id ascending among ties
-    order = sorted(range(N), key=lambda e: (-loads[e], e))
-    # native / pending / assigned load per device
-    g_n = [sum(loads[d * M:(d + 1) * M]) for d in range(P)]
-    g_p = list(g_n)
-    g_a = [0] * P
+    ledger = DeviceLedger([sum(loads[d * M:(d + 1) * M]) for d in range(P)], cap)
     assignments: Dict[int, List[Tuple[int, int, int]]] = {}
     forced = 0
-    for i in order:
-        e = loads[i]
-        ng = i // M
-        g_p[ng] -= e
-        na = cap - g_a[ng] - g_p[ng]  # room left on the native device
-        A: List[Tuple[int, int, int]] = []
-        if na >= e:
-            # Case 1: the native device takes the whole expert
-            A.append((ng, 0, e))
-            g_a[ng] += e
-        elif na > 0:
-            # Case 2: native takes what fits, the rest spills
-            nc = min(na, e)
-            A.append((ng, 0, nc))
-            g_a[ng] += nc
-            forced += least_loaded_spill(ng, e - nc, nc, A, g_a, g_p,
-                                         cap, m, P)
-        else:
-            # Case 3: native device already full, spill the whole expert
-            forced += least_loaded_spill(ng, e, 0, A, g_a, g_p, cap, m, P)
-        assignments[i] = [(d, s, t) for (d, s, t) in A if t > s]
+    for e in sorted(range(N), key=lambda i: (-loads[i], i)):
+        home = e // M
+        ledger.pending[home] -= loads[e]
+        keep = min(loads[e], max(0, ledger.free(home)))
+        pieces: List[Tuple[int, int, int]] = []
+        if keep > 0:
+            pieces.append((home, 0, keep))
+            ledger.give(home, keep)
+        if loads[e] > keep:
+            spilled, f = spill_to_least_loaded(ledger, home, loads[e] - keep, keep, m)
+            pieces += spilled
+            forced += f
+        assignments[e] = [(d, s, t) for (d, s, t) in pieces if t > s]
     transfers = sorted({(e, e // M, d)
-                        for e, chunks in assignments.items()
-                        for (d, s, t) in chunks if d != e // M})
+                        for e, pieces in assignments.items()
+                        for (d, s, t) in pieces if d != e // M})
     return assignments, transfers, forced
 
 
@@ -316,7 +342,7 @@ def plan(ids_flat: Sequence[int], E: int, P: int, cap: int, m: int = 1,
 
 
 # ---------------------------------------------------------------------------
-# Step 3: the permutation (Sec. 2.1 re-indexing; Alg. 4 sort/index_select)
+# Step 3: the permutation (Sec. 2.1 re-indexing; Alg. 4 sorting and gathering)
 # ---------------------------------------------------------------------------
 
 def pair_ranks(ids_flat: Sequence[int], E: int) -> List[int]:
@@ -426,6 +452,32 @@ def combine(pair_out: np.ndarray, gates: np.ndarray) -> np.ndarray:
     pair_out[t, k] (float64). pair_out: T x K x D; gates: T x K."""
     return np.einsum("tk,tkd->td", np.asarray(gates, dtype=np.float64),
                      np.asarray(pair_out, dtype=np.float64))
+
+
+# ---------------------------------------------------------------------------
+# Per-device peak memory of a plan (Sec. 3.2, Eq. 4)
+# ---------------------------------------------------------------------------
+
+def m_local(groups: Sequence[Tuple[int, int, int, int]], P: int, D: int, F: int,
+            matrices: int = 3) -> List[int]:
+    """Eq. (4): the peak memory of the MoE layer on one device, in elements,
+    M_local = sum over the device's groups i of (B_i D + matrices D H + B_i H),
+    with B_i the group's rows (token-expert pairs), H = F the expert's hidden
+    size and `matrices` weight matrices of D x H per expert.
+
+    Eq. (4) counts one D x H matrix per expert; the SwiGLU expert of
+    Sec. 5.1 has three (gate, up, down), so the default is 3, and
+    matrices=1 gives Eq. (4) as printed. Each group is one (device, expert)
+    GEMM problem, so a spilled expert counts its weights once on every
+    device that holds a piece of it.
+
+    groups: (device, expert, row_start, n) rows of a plan. Returns a list of
+    P element counts.
+    """
+    out = [0] * P
+    for (d, _e, _r0, n) in groups:
+        out[int(d)] += int(n) * D + matrices * D * F + int(n) * F
+    return out
 
 
 # ---------------------------------------------------------------------------

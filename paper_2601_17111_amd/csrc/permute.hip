@@ -1,6 +1,6 @@
 // Step 3 of the LLEP hot path: permute token-expert pairs into their rows.
 //
-// Order (Sec. 2.1 re-indexing; Alg. 4 sort / index_select / build chunks):
+// Order (Sec. 2.1 re-indexing; Alg. 4 sorting, gathering, chunk building):
 // pair p of expert e has rank r = number of earlier pairs of e. It lies in the
 // chunk (d, e, s, t) of the plan with s <= r < t, and goes to row
 // chunk_row + (r - s).

@@ -1,7 +1,7 @@
 // Steps 1-2 of the LLEP hot path: the routing histogram and the plan.
 //
 // hist_kernel   counts, per rank tile of kRankTile pairs, how many pairs go
-//               to each expert (Alg. 4, "sum of loads of global experts").
+//               to each expert (Alg. 4, first step: the global per-expert loads).
 // plan_kernel   one workgroup: scans the tile counts into per-tile rank bases
 //               and the loads l, runs the lambda test (Alg. 4), then the
 //               least-loaded assignment (Alg. 2 with the spill loop of

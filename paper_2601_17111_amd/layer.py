@@ -4,9 +4,22 @@ sequencing only; all arithmetic happens in the library's kernels."""
 
 from __future__ import annotations
 
-from typing import Optional
+from typing import List, Optional, Sequence
 
 from . import binding as B
+
+
+def m_local_bytes(groups: Sequence[Sequence[int]], P: int, D: int, F: int,
+                  elem_bytes: int) -> List[int]:
+    """Peak-memory model of each device's share (Sec. 3.2, Eq. 4) from a
+    plan's group table: for every group (device, expert, row_start, n) its
+    n x D token rows, the expert's three D x F SwiGLU matrices and its n x F
+    intermediate, in bytes of `elem_bytes` per element."""
+    out = [0] * P
+    for g in groups:
+        d, n = int(g[0]), int(g[3])
+        out[d] += (n * (D + F) + 3 * D * F) * elem_bytes
+    return out
 
 
 class LLEPLayer:

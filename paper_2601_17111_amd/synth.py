@@ -19,6 +19,8 @@ models):
                their K distinct slots to expert 0; every other slot is a
                distinct uniform expert;
     - "balanced": exactly R/E pairs per expert, shuffled (R % E == 0);
+    - "loads":  exactly the given number of pairs per expert, shuffled
+               (the counts sum to T*K);
 * gates: softmax over K i.i.d. N(0, 1) logits per token, float32;
 * x: N(0, 1), rounded to bfloat16 (round-to-nearest-even) for bf16 layers;
 * weights: N(0, 0.02^2) per expert, drawn with torch's generator on the
@@ -145,6 +147,10 @@ def draw_ids(cfg: LayerConfig, rng: np.random.Generator) -> np.ndarray:
         R = T * K
         assert R % E == 0
         ids = rng.permutation(np.repeat(np.arange(E), R // E))
+    elif kind == "loads":
+        counts = np.asarray(cfg.routing[1], dtype=np.int64)
+        assert len(counts) == E and counts.sum() == T * K
+        ids = rng.permutation(np.repeat(np.arange(E), counts))
     else:
         raise ValueError(kind)
     return np.ascontiguousarray(ids.reshape(T, K).astype(np.int32))

@@ -71,6 +71,24 @@ def rel_err(got: np.ndarray, want: np.ndarray) -> float:
     return float(np.abs(got.astype(np.float64) - want).max() / (den if den > 0 else 1.0))
 
 
+def elementwise_rel_err(got: np.ndarray, want: np.ndarray) -> float:
+    """Diagnostic, not a bound: max over entries of |got - want| / max(|want|,
+    1e-3 max |want|), the per-element relative error with entries near zero
+    measured against a floor of a thousandth of the largest one."""
+    want = np.asarray(want, dtype=np.float64)
+    den = np.maximum(np.abs(want), 1e-3 * max(np.abs(want).max(), 1e-300))
+    return float((np.abs(got.astype(np.float64) - want) / den).max())
+
+
+def report(tag: str, got: np.ndarray, want: np.ndarray) -> float:
+    """Print the bound's relative error and the element-wise diagnostic;
+    returns the former."""
+    err = rel_err(got, want)
+    print(f"[{tag}] max-norm rel err {err:.3e}, element-wise rel err "
+          f"{elementwise_rel_err(got, want):.3e}", flush=True)
+    return err
+
+
 class LayerRun:
     """Inputs on the GPU, packed weights, and one LLEPLayer."""
 

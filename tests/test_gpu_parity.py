@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 from conftest import GOLDEN
-from gpu_util import LayerRun, assert_plan_equal, device, rel_err, run_plan
+from gpu_util import LayerRun, assert_plan_equal, device, rel_err, report, run_plan
 
 pytestmark = pytest.mark.gpu
 
@@ -208,14 +208,24 @@ def _check_layer(run, tol, tokens=None):
     ref = oracle.plan(inp.ids.reshape(-1).tolist(), cfg.E, cfg.P, cfg.capacity, cfg.min_chunk,
                       lam=cfg.lam)
     info = run.layer.bufs.info_dict()
-    assert info["n_groups"] == len(ref.groups)
-    assert run.layer.bufs.groups[:len(ref.groups)].cpu().tolist() == [list(g) for g in ref.groups]
+    b = run.layer.bufs
+    nc, ng, nx = info["n_chunks"], info["n_groups"], info["n_xfers"]
+    got = dict(
+        loads=b.loads.cpu().tolist(),
+        chunks=[tuple(c) for c in b.chunks[:nc].cpu().tolist()],
+        chunk_row=b.chunk_row[:nc].cpu().tolist(),
+        expert_chunk_begin=b.expert_chunk_begin.cpu().tolist(),
+        groups=[tuple(g) for g in b.groups[:ng].cpu().tolist()],
+        group_begin=b.group_begin.cpu().tolist(),
+        device_rows=b.device_rows.cpu().tolist(),
+        transfers=[tuple(x) for x in b.xfers[:nx].cpu().tolist()])
+    assert_plan_equal(got, info, ref)
     pr_ref, rp_ref = oracle.permute(inp.ids.reshape(-1).tolist(), ref, cfg.E)
     assert np.array_equal(run.layer.pair_row.cpu().numpy(), pr_ref)
     W = run.host_weights(range(cfg.E))
     toks = list(range(cfg.T)) if tokens is None else tokens
     want = oracle.moe_output(inp.x, inp.ids, inp.gates, lambda e: W.get(e), toks)
-    err = rel_err(y[toks], want)
+    err = report(f"{cfg.name} y", y[toks], want)
     assert err <= tol, f"relative error {err:.3e} > {tol}"
     # out_perm rows against the per-row expert function
     rows = np.linspace(0, sum(ref.device_rows) - 1, num=min(64, sum(ref.device_rows))).astype(int)

@@ -17,9 +17,10 @@ import pytest
 from hypothesis import given, settings, strategies as st
 
 from conftest import GOLDEN
-from oracle import (bypass_to_standard_ep, capacity_from_alpha, expert_loads,
-                    least_loaded_assignment, min_max_load_exhaustive, pair_ranks,
-                    permute, plan, standard_ep_assignment)
+from oracle import (DeviceLedger, bypass_to_standard_ep, capacity_from_alpha,
+                    expert_loads, least_loaded_assignment, m_local,
+                    min_max_load_exhaustive, pair_ranks, permute, plan,
+                    spill_to_least_loaded, standard_ep_assignment)
 
 
 def _load(name):
@@ -213,6 +214,118 @@ def test_exhaustive_optimum():
             for (d, s, t) in cs:
                 rows[d] += t - s
         assert opt <= max(rows) <= cap
+
+
+@pytest.mark.parametrize("case", _load("exhaustive_min_foreign.json")["cases"],
+                         ids=lambda c: c["name"].split(":")[0])
+def test_exhaustive_min_foreign_hand_cases(case):
+    """The exhaustive search's optimum and its fewest foreign (expert, device)
+    shares under a cap, against cases worked by hand."""
+    opt, min_foreign = min_max_load_exhaustive(case["loads"], case["P"], case["M"], case["cap"])
+    assert opt == case["opt"]
+    assert min_foreign == case["min_foreign"]
+
+
+def test_lla_transfers_not_below_exhaustive_minimum():
+    """LLA's weight transfers under cap = ceil(R/P) are never fewer than the
+    exhaustive minimum of foreign shares that meet the same cap (a lower
+    bound; native-first keeps them low, Sec. 4 Elaboration)."""
+    rng = random.Random(3)
+    cases = 0
+    while cases < 40:
+        P = rng.choice([2, 3])
+        M = rng.choice([1, 2]) if P == 2 else 1
+        loads = [rng.randint(0, 6) for _ in range(P * M)]
+        R = sum(loads)
+        if R == 0:
+            continue
+        cases += 1
+        cap = math.ceil(R / P) + rng.randint(0, 2)
+        _, W, forced = least_loaded_assignment(loads, M, cap, 1)
+        _, min_foreign = min_max_load_exhaustive(loads, P, M, cap)
+        assert forced == 0 and min_foreign is not None
+        assert len(W) >= min_foreign
+
+
+def test_spill_step_alone():
+    """Alg. 3 on its own, traced by hand: three other devices with
+    occupancies 5, 2, 2 under cap 6 and m = 2. Round 1 ranks (1: 2, 2: 2,
+    3: 5); device 1 has room 4 >= m and takes 4 of the 7 pairs. Round 2
+    ranks (2: 2, 3: 5, 1: 6); device 2 has room 4 and takes the last 3."""
+    ledger = DeviceLedger([9, 2, 2, 5], 6)  # device 0 is the expert's home
+    ledger.pending[0] = 0
+    ledger.placed[0] = 6
+    pieces, forced = spill_to_least_loaded(ledger, 0, 7, 6, 2)
+    assert pieces == [(1, 6, 10), (2, 10, 13)] and forced == 0
+    assert ledger.placed == [6, 4, 3, 0]
+    # every other device has a gap smaller than m and smaller than what is
+    # left: the emptiest one takes all of it (a force-assignment)
+    ledger = DeviceLedger([0, 5, 5, 4], 6)
+    pieces, forced = spill_to_least_loaded(ledger, 0, 5, 0, 3)
+    assert pieces == [(3, 0, 5)] and forced == 1
+    # a gap smaller than m is still taken when it holds everything left
+    ledger = DeviceLedger([0, 5, 4, 4], 6)
+    pieces, forced = spill_to_least_loaded(ledger, 0, 2, 3, 3)
+    assert pieces == [(2, 3, 5)] and forced == 0
+
+
+def test_m_local_worked_example():
+    """Eq. 4 worked by hand on the groups of hand trace H1."""
+    g = _load("m_local_example.json")
+    for c in g["cases"]:
+        assert m_local(g["groups"], g["P"], g["D"], g["F"], c["matrices"]) == c["m_local"]
+
+
+def test_m_local_properties():
+    """Eq. 4 summed over the devices: every row counts its D + F elements
+    once, and every group its weights once; under standard EP a device's
+    figure is its native groups' only, so an overloaded device shows the
+    memory spike the paper describes (Sec. 3.2), and LLEP lowers the
+    maximum."""
+    rng = np.random.default_rng(4)
+    E, P, D, F = 16, 4, 8, 12
+    ids = np.where(rng.random(4000) < 0.7, 0, rng.integers(1, E, 4000)).tolist()
+    cap = capacity_from_alpha(len(ids), Fraction(1), P)
+    pl = plan(ids, E, P, cap, 1)
+    ep = plan(ids, E, P, cap, 1, mode="ep")
+    for p in (pl, ep):
+        got = m_local(p.groups, P, D, F)
+        assert sum(got) == len(ids) * (D + F) + 3 * D * F * len(p.groups)
+        for d in range(P):
+            mine = [g for g in p.groups if g[0] == d]
+            assert got[d] == sum(n * (D + F) for (_, _, _, n) in mine) + 3 * D * F * len(mine)
+    assert max(m_local(pl.groups, P, D, F)) < max(m_local(ep.groups, P, D, F))
+
+
+def test_synth_capacity_matches_oracle():
+    """The layer shapes' capacities (drawn with the inputs) equal Alg. 2's
+    m_alpha as the oracle computes it, for all five layer shapes."""
+    from paper_2601_17111_amd.synth import CONFIGS, gpt_oss_120b
+    cfgs = list(CONFIGS.values()) + [gpt_oss_120b(k) for k in (16, 4, 1)]
+    want = {"tiny-fp32": 160, "gpt-oss-20b": 9012, "gpt-oss-120b": 18023,
+            "qwen3-30b-a3b": 72090, "deepseek-v3": 8192}
+    for c in cfgs:
+        assert c.capacity == capacity_from_alpha(c.R, c.alpha, c.P), c.name
+        assert c.capacity == want[c.name.split("-hot")[0]], c.name
+
+
+def test_package_m_local_matches_oracle():
+    """The benchmark's per-device memory report (a function of the plan's
+    group table in the package) equals the oracle's Eq. 4 on oracle plans."""
+    from paper_2601_17111_amd.layer import m_local_bytes
+    rng = np.random.default_rng(9)
+    for mode in ("llep", "ep"):
+        for trial in range(4):
+            E, P = 32, 8
+            ids = np.where(rng.random(3000) < 0.5, rng.integers(0, 4, 3000),
+                           rng.integers(0, E, 3000)).tolist()
+            cap = capacity_from_alpha(len(ids), Fraction(11, 10), P)
+            pl = plan(ids, E, P, cap, 1, mode=mode)
+            D, F = 64 * (trial + 1), 96
+            for eb in (2, 4):
+                got = m_local_bytes(pl.groups, P, D, F, eb)
+                want = [v * eb for v in m_local(pl.groups, P, D, F)]
+                assert got == want
 
 
 # --------------------------------------------------------------------------
