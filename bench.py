@@ -6,12 +6,16 @@ grouped SwiGLU FFN of the most-loaded virtual device's groups -> combine.
 Inputs are resident in HBM before timing starts; the most-loaded device d* is
 read from the plan once, before timing (the batch does not change).
 
+Timing: every timed step follows a 512 MiB cache-flush write (outside the
+step's events, so no step finds the previous one's operands in the L2s or the
+256 MB MALL); the reported times are medians over the timed steps of HIP
+events on the stream, with their spread.
+
 Prints one JSON line. `value` is tokens per second of the measured step
-(T / time per step). The `roofline` object is for the grouped FFN (two MFMA
-GEMM kernels plus a tiny tile-list kernel): algorithmic flops 6*D*F per row of
-d*, over the average duration of that call measured with HIP events on its
-stream. `cpu_baseline` times the CPU oracle on a bounded sample of the same
-workload.
+(T / median time per step). The `roofline` object is for the grouped FFN:
+algorithmic flops 6*D*F per row of d*, over the median duration of that call
+measured with HIP events on its stream. `cpu_baseline` times the CPU oracle on
+a bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
@@ -38,7 +42,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "grouped_ffn_traffic.json")
 def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt-oss-120b-hot1")
     ap.add_argument("--seed", type=int, default=0)
@@ -125,14 +129,47 @@ def _m_local_gb(layer, P, D, F, eb):
     return [v / 1e9 for v in m_local_bytes(groups, P, D, F, eb)]
 
 
-def _time_steps(layer, run, steps, dstar):
-    """Run `steps` steps; per-segment HIP event times (ms) on the stream."""
+FLUSH_BYTES = 512 << 20  # written between timed reps: twice the 256 MB MALL
+
+
+class _Flush:
+    """A device buffer of FLUSH_BYTES, overwritten before each timed rep so
+    that no rep finds its operands in the L2s or the MALL from the previous
+    one (the write is outside the timed events)."""
+
+    def __init__(self, dev):
+        import torch
+        self.buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+        self.i = 0
+
+    def __call__(self):
+        self.i += 1
+        self.buf.fill_(self.i & 0xFF)
+
+
+def _stats(vals):
+    """Median and spread of a list of per-rep times (ms)."""
+    v = sorted(vals)
+    n = len(v)
+
+    def q(f):
+        return v[min(n - 1, int(round(f * (n - 1))))]
+    return {"median": q(0.5), "mean": sum(v) / n, "min": v[0], "p10": q(0.1), "p90": q(0.9),
+            "max": v[-1], "reps": n}
+
+
+def _time_steps(layer, run, steps, dstar, flush=None, spread=None):
+    """Run `steps` steps, each after a cache-flush write (outside its
+    events); per-segment HIP event times (ms) on the stream. Returns the
+    median step time and the per-segment medians; `spread`, if a dict, gets
+    the statistics of the step and segment times."""
     import torch
-    seg = {"plan": 0.0, "permute": 0.0, "grouped_ffn": 0.0, "combine": 0.0}
+    names = ("plan", "permute", "grouped_ffn", "combine")
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for i in range(steps):
+        if flush is not None:
+            flush()
         e = ev[i]
         e[0].record()
         layer.plan(run["ids"])
@@ -144,14 +181,16 @@ def _time_steps(layer, run, steps, dstar):
         layer.combine(run["gates"])
         e[4].record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    for e in ev:
-        for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
-            seg[k] += a.elapsed_time(b) / steps
-    return wall * 1e3 / steps, seg
+    per = {k: [e[j].elapsed_time(e[j + 1]) for e in ev] for j, k in enumerate(names)}
+    tot = [e[0].elapsed_time(e[4]) for e in ev]
+    if spread is not None:
+        spread["step"] = _stats(tot)
+        for k in names:
+            spread[k] = _stats(per[k])
+    return _stats(tot)["median"], {k: _stats(per[k])["median"] for k in names}
 
 
-def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps):
+def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps, flush):
     """The backward of the step on the most-loaded device's share: combine
     backward (all tokens) -> grouped SwiGLU backward of d*'s groups (input
     gradients of its rows and its partial weight gradients) from the gate /
@@ -184,29 +223,33 @@ def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps):
         e[3].record()
 
     def timed(gate_up):
-        seg = {"combine_backward": 0.0, "grouped_ffn_backward": 0.0, "dx_sum": 0.0}
+        names = ("combine_backward", "grouped_ffn_backward", "dx_sum")
+        per = {k: [] for k in names}
         for i in range(steps + 2):
+            flush()
             e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
             step(gate_up, e)
             torch.cuda.synchronize()
             if i >= 2:
-                for k, (a, b) in zip(seg, zip(e[:-1], e[1:])):
-                    seg[k] += a.elapsed_time(b) / steps
-        return seg
+                for k, (a, b) in zip(names, zip(e[:-1], e[1:])):
+                    per[k].append(a.elapsed_time(b))
+        return {k: _stats(v)["median"] for k, v in per.items()}
 
     seg = timed(L.gate_up)
     recompute_ms = timed(None)["grouped_ffn_backward"]
     # the training forward's grouped FFN on d*: the inference one plus the
     # stores of gate / up
-    train_ms = 0.0
+    train = []
     for i in range(steps + 2):
+        flush()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         L.ffn(run["gu"], run["dn"], dstar, save_gate_up=True)
         b.record()
         torch.cuda.synchronize()
         if i >= 2:
-            train_ms += a.elapsed_time(b) / steps
+            train.append(a.elapsed_time(b))
+    train_ms = _stats(train)["median"]
     D, F, T, K = cfg.D, cfg.F, cfg.T, cfg.K
     R = T * K
     t_ffn = seg["grouped_ffn_backward"] * 1e-3
@@ -314,7 +357,8 @@ def _sweep(args):
         for frac in (0.3, 0.5, 0.8, 0.95):
             for T in (4096, 8192, 16384, 32768, 65536):
                 points.append(("batch", base.with_(T=T, routing=("hot", frac, 4))))
-    steps = max(3, args.steps // 4)
+    steps = max(5, args.steps // 4)
+    flush = _Flush(dev)
     for kind, cfg in points:
         inp = make_inputs(cfg, args.seed)
         run = dict(ids=torch.from_numpy(inp.ids).to(dev), gates=torch.from_numpy(inp.gates).to(dev),
@@ -331,7 +375,7 @@ def _sweep(args):
             for _ in range(2):
                 layer.plan(run["ids"]); layer.permute(run["ids"], run["gates"], run["x"])
                 layer.ffn(gu, dn, d); layer.combine(run["gates"])
-            _, seg = _time_steps(layer, run, steps, d)
+            _, seg = _time_steps(layer, run, steps, d, flush)
             model = seg["plan"] + (seg["permute"] + seg["combine"]) / cfg.P + seg["grouped_ffn"]
             res[mode] = {"max_device_rows": rows, "bypassed": info["bypassed"],
                          "forced": info["forced"], "n_xfers": info["n_xfers"],
@@ -361,7 +405,8 @@ def _sweep_experts(args):
     B.lib()
     dev = "cuda:0"
     T, D, F = 65536, 8192, 8192
-    reps = max(3, args.steps // 4)
+    reps = max(5, args.steps // 4)
+    flush = _Flush(dev)
     for N in (4, 16, 32, 64, 128, 256):
         cfg = LayerConfig(f"a1-n{N}", T=T, D=D, F=F, E=N, K=1, P=1, alpha=Fraction(1),
                           dtype="bf16", routing=("balanced",))
@@ -384,6 +429,7 @@ def _sweep_experts(args):
         torch.cuda.synchronize()
         ts = []
         for _ in range(reps):
+            flush()
             s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             s.record()
             layer.ffn(gu, dn, -1)
@@ -459,12 +505,18 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    flush = _Flush(dev)
     for _ in range(args.warmup):
+        flush()
         layer.plan(run["ids"])
         layer.permute(run["ids"], run["gates"], run["x"])
         layer.ffn(run["gu"], run["dn"], dstar)
         layer.combine(run["gates"])
-    ms, seg = _time_steps(layer, run, args.steps, dstar)
+    spread = {}
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    ms, seg = _time_steps(layer, run, args.steps, dstar, flush, spread)
+    t_wall = time.perf_counter() - t_wall
 
     D, F, T, K = cfg.D, cfg.F, cfg.T, cfg.K
     eb = 2 if cfg.dtype == "bf16" else 4
@@ -501,6 +553,9 @@ def main():
             "flops_per_launch": flops,
         },
         "segments_ms": seg,
+        "timing": {"statistic": "median over the timed steps of HIP-event times on the stream",
+                   "flush_bytes_between_steps": FLUSH_BYTES, "spread_ms": spread,
+                   "wall_s_incl_flushes": t_wall},
         "plan": {"max_device": dstar, "device_rows": dev_rows, "capacity": cfg.capacity,
                  "n_chunks": info["n_chunks"], "n_groups": info["n_groups"],
                  "n_xfers": info["n_xfers"]},
@@ -519,7 +574,7 @@ def main():
 
     # the raw 1-GPU layer: all P devices' groups back to back in one call
     if not args.no_full_layer:
-        ms_full, seg_full = _time_steps(layer, run, max(3, args.steps // 4), -1)
+        ms_full, seg_full = _time_steps(layer, run, max(5, args.steps // 3), -1, flush)
         total_rows = sum(dev_rows)
         out["full_layer_all_devices"] = {
             "ms_per_step": ms_full, "tokens_per_s": T / (ms_full * 1e-3), "segments_ms": seg_full,
@@ -529,7 +584,7 @@ def main():
 
     if cfg.dtype == "bf16" and not args.no_backward:
         out["backward"] = _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows,
-                                    max(3, args.steps // 2))
+                                    max(5, args.steps // 2), flush)
 
     if not args.no_ep:
         layer.set_mode("ep")
@@ -541,7 +596,7 @@ def main():
         layer.permute(run["ids"], run["gates"], run["x"])
         for _ in range(2):
             layer.ffn(run["gu"], run["dn"], d_ep)
-        ms_ep, seg_ep = _time_steps(layer, run, max(3, args.steps // 4), d_ep)
+        ms_ep, seg_ep = _time_steps(layer, run, max(5, args.steps // 3), d_ep, flush)
         out["standard_ep"] = {
             "max_device": d_ep, "max_device_rows": rows_ep[d_ep], "ms_per_step": ms_ep,
             "segments_ms": seg_ep,
