@@ -228,6 +228,35 @@ int llep_grouped_ffn_train(const llep_plan_params *params,
                            void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/* Bytes of the device array that the library holds on every GPU it runs on
+ * (until the process ends) as the workspace of llep_grouped_ffn_noalloc. */
+#define LLEP_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* llep_grouped_ffn for callers that cannot allocate device memory: code
+ * under HIP graph capture, serving loops and harnesses that forbid hipMalloc.
+ * The same kernels as llep_grouped_ffn with the same arguments, except that
+ * the workspace is the library's own LLEP_NOALLOC_SCRATCH_BYTES array on the
+ * current GPU instead of a caller buffer; out_perm is bit-identical to
+ * llep_grouped_ffn's. The call allocates and frees nothing; what the kernels
+ * need zeroed in the array they clear themselves (no memset node).
+ * Requires llep_grouped_ffn_workspace_bytes(params, F, dtype) <=
+ * LLEP_NOALLOC_SCRATCH_BYTES (for bf16 roughly (T*K + 16 (2E + P)) * F * 2
+ * bytes), else LLEP_E_WORKSPACE and nothing is enqueued.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents: calls on one stream are ordered and safe, but calls that overlap
+ * on one GPU (other streams, other threads without ordering) race and give
+ * undefined results. The first call on a GPU looks up the array's address
+ * there (with that GPU current) and keeps it; make that first call outside
+ * graph capture.
+ * Errors: as llep_grouped_ffn (LLEP_E_WORKSPACE: too large for the array),
+ * LLEP_E_HIP when the array's address cannot be obtained. */
+int llep_grouped_ffn_noalloc(const llep_plan_params *params,
+                             const llep_plan_buffers *plan, int32_t device,
+                             const void *x_perm, const void *w_gate_up_packed,
+                             const void *w_down_packed, int32_t D, int32_t F,
+                             llep_dtype dtype, void *out_perm,
+                             hipStream_t stream);
+
 /* Step 5. y[t] = sum over k = 0..K-1 (ascending) of
  *   topk_gates[t*K+k] * out_perm[pair_row[t*K+k]]
  * in float32, rounded once to dtype; pairs with pair_row < 0 are skipped.

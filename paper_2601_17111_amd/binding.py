@@ -35,8 +35,9 @@ EXPORTED = [
     "llep_grouped_ffn_workspace_bytes", "llep_packed_gate_up_bytes",
     "llep_packed_down_bytes", "llep_last_error", "llep_combine_backward",
     "llep_pack_weights_backward", "llep_grouped_ffn_backward_workspace_bytes",
-    "llep_grouped_ffn_backward", "llep_grouped_ffn_train",
+    "llep_grouped_ffn_backward", "llep_grouped_ffn_train", "llep_grouped_ffn_noalloc",
 ]
+LLEP_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class llep_plan_params(ctypes.Structure):
@@ -96,6 +97,8 @@ def lib() -> ctypes.CDLL:
                                                 ctypes.c_int, _P, _P, sz, _P]),
             "llep_grouped_ffn_train": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, i32, i32,
                                                       ctypes.c_int, _P, _P, _P, sz, _P]),
+            "llep_grouped_ffn_noalloc": (ctypes.c_int, [pp, pb, i32, _P, _P, _P, i32, i32,
+                                                        ctypes.c_int, _P, _P]),
             "llep_combine": (ctypes.c_int, [pp, _P, _P, _P, i32, ctypes.c_int, _P, _P]),
             "llep_combine_backward": (ctypes.c_int, [pp, _P, _P, _P, _P, i32, ctypes.c_int, _P,
                                                      _P, _P]),
@@ -264,6 +267,18 @@ def llep_grouped_ffn_train(params: llep_plan_params, bufs: PlanBuffers, device: 
                                         _ptr(workspace),
                                         workspace.numel() * workspace.element_size(),
                                         _stream(stream)), "llep_grouped_ffn_train")
+
+
+def llep_grouped_ffn_noalloc(params: llep_plan_params, bufs: PlanBuffers, device: int, x_perm,
+                             w_gate_up, w_down, out_perm, stream=None):
+    """llep_grouped_ffn with the library's own workspace array (no caller
+    workspace; at most LLEP_NOALLOC_SCRATCH_BYTES)."""
+    D = x_perm.shape[-1]
+    F = w_down.shape[-1]
+    _check(lib().llep_grouped_ffn_noalloc(ctypes.byref(params), ctypes.byref(bufs.struct),
+                                          device, _ptr(x_perm), _ptr(w_gate_up), _ptr(w_down),
+                                          D, F, _dtype_code(x_perm), _ptr(out_perm),
+                                          _stream(stream)), "llep_grouped_ffn_noalloc")
 
 
 def llep_combine(params: llep_plan_params, out_perm, pair_row, topk_gates, y, stream=None):

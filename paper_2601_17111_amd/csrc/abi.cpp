@@ -1,6 +1,7 @@
 // C ABI of the LLEP hot path: argument checks on the host, then launches.
-// No entry point allocates, synchronizes or keeps state between calls
-// (apart from the calling thread's last error text).
+// No entry point allocates, synchronizes or keeps state between calls, apart
+// from the calling thread's last error text and the per-GPU address of the
+// library's workspace array (llep_grouped_ffn_noalloc), looked up once.
 #include <stdint.h>
 #include <string.h>
 
@@ -234,6 +235,28 @@ int llep_grouped_ffn_train(const llep_plan_params *params, const llep_plan_buffe
   return grouped_ffn(params, plan, device, x_perm, w_gate_up_packed, w_down_packed, D, F, dtype,
                      out_perm, gate_up, workspace, workspace_bytes, stream,
                      "llep_grouped_ffn_train");
+}
+
+int llep_grouped_ffn_noalloc(const llep_plan_params *params, const llep_plan_buffers *plan,
+                             int32_t device, const void *x_perm, const void *w_gate_up_packed,
+                             const void *w_down_packed, int32_t D, int32_t F, llep_dtype dtype,
+                             void *out_perm, hipStream_t stream) {
+  int rc = check_params(params);
+  if (rc != LLEP_OK) return rc;
+  if (F < 1 || elem_bytes(dtype) == 0) return check_ffn_dims(D, F, dtype);
+  const size_t need = llep::ffn_workspace_bytes(params->T * params->K, params->E, params->P, F, dtype);
+  if (need > size_t(LLEP_NOALLOC_SCRATCH_BYTES))
+    return fail(LLEP_E_WORKSPACE,
+                "llep_grouped_ffn_noalloc: this layer needs " + std::to_string(need) +
+                    " bytes of workspace, more than the library's LLEP_NOALLOC_SCRATCH_BYTES = " +
+                    std::to_string(size_t(LLEP_NOALLOC_SCRATCH_BYTES)) +
+                    "; use llep_grouped_ffn with a caller workspace");
+  void *ws = nullptr;
+  const hipError_t err = llep::ffn_scratch_address(&ws);
+  if (err != hipSuccess) return hip_result(err, "llep_grouped_ffn_noalloc (scratch address)");
+  return grouped_ffn(params, plan, device, x_perm, w_gate_up_packed, w_down_packed, D, F, dtype,
+                     out_perm, nullptr, ws, size_t(LLEP_NOALLOC_SCRATCH_BYTES), stream,
+                     "llep_grouped_ffn_noalloc");
 }
 
 int llep_combine(const llep_plan_params *params, const void *out_perm, const int32_t *pair_row,

@@ -9,6 +9,8 @@
 // This file: the tile list, the forward launcher, the float32 forward (one
 // thread per output element, reference precision, no matrix cores) and the
 // weight packing. The GEMM kernel itself is in gemm.h.
+#include <mutex>
+
 #include "gemm.h"
 
 namespace llep {
@@ -210,6 +212,37 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
                      static_cast<float *>(a.out_perm), a.groups, a.group_begin, a.device, a.P,
                      a.D, a.F);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// The library's own workspace for callers that cannot allocate
+// (llep_grouped_ffn_noalloc): one array per GPU, held until the process ends.
+// On the host `scratch` names a stand-in, not a device address: its address
+// on a GPU comes from hipGetSymbolAddress with that GPU current, looked up
+// once per GPU and kept; the kernels get that address, never the name.
+// ---------------------------------------------------------------------------
+
+static __device__ __align__(256) char scratch[LLEP_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxGpus = 64;
+
+hipError_t ffn_scratch_address(void **ptr) {
+  static std::mutex mu;
+  static void *addr[kMaxGpus] = {};
+  int dev = -1;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= kMaxGpus) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void *p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return err;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 // ---------------------------------------------------------------------------

@@ -76,6 +76,9 @@ struct FfnArgs {
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t F,
                            llep_dtype dtype);
 hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream);
+// Address on the current GPU of the library's LLEP_NOALLOC_SCRATCH_BYTES
+// workspace array (looked up once per GPU, then cached).
+hipError_t ffn_scratch_address(void **ptr);
 
 struct FfnBwdArgs {
   int64_t R;
