@@ -12,7 +12,8 @@ step's events, so no step finds the previous one's operands in the L2s or the
 events on the stream, with their spread.
 
 Prints one JSON line. `value` is tokens per second of the measured step
-(T / median time per step). The `roofline` object is for the grouped FFN:
+(T / median time per step). The `roofline` object is for the grouped FFN
+(a tiny tile-list kernel, then one persistent launch for both projections):
 algorithmic flops 6*D*F per row of d*, over the median duration of that call
 measured with HIP events on its stream. `cpu_baseline` times the CPU oracle on
 a bounded sample of the same workload.
@@ -549,7 +550,8 @@ def main():
         "roofline": {
             "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": tflops / PEAK_BF16_TFLOPS, "traffic": traffic,
-            "kernel": "llep_grouped_ffn on the most-loaded device (tile_table_kernel + gemm256_kernel x2)",
+            "kernel": ("llep_grouped_ffn on the most-loaded device (tile_table_kernel + "
+                       "ffn_fused_kernel: both projections in one persistent launch)"),
             "flops_per_launch": flops,
         },
         "segments_ms": seg,

@@ -82,6 +82,11 @@ extern "C" {
 
 /* ---- device-detected status bits (llep_plan_info.status) ---------------- */
 #define LLEP_STATUS_BAD_EXPERT_ID 1 /* an id outside [0, E): pair ignored */
+#define LLEP_STATUS_FFN_WAIT 2      /* set by the bf16 grouped FFN when a
+                                       down-projection tile gave up waiting
+                                       (about a second) for its activations;
+                                       never expected, the call's outputs are
+                                       then undefined */
 
 /* ---- limits --------------------------------------------------------------- */
 #define LLEP_MAX_EXPERTS 512

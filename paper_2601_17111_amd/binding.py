@@ -25,6 +25,7 @@ LLEP_BF16 = 1
 LLEP_MODE_LLEP = 0
 LLEP_MODE_EP = 1
 LLEP_STATUS_BAD_EXPERT_ID = 1
+LLEP_STATUS_FFN_WAIT = 2
 LLEP_MAX_EXPERTS = 512
 LLEP_MAX_DEVICES = 64
 LLEP_MAX_FFN_DIM = 65536

@@ -213,6 +213,7 @@ static int grouped_ffn(const llep_plan_params *params, const llep_plan_buffers *
   a.gate_up_out = gate_up;
   a.ws = workspace;
   a.ws_bytes = workspace_bytes;
+  a.status = &plan->info->status;
   return hip_result(llep::launch_grouped_ffn(a, stream), name);
 }
 

@@ -150,6 +150,9 @@ __device__ __forceinline__ void dma16(const char *base_in, int32_t voff, uint32_
   const uint32_t lo = uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(bv)));
   const uint32_t hi = uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(bv >> 32)));
   const uint64_t base = (uint64_t(hi) << 32) | uint64_t(lo);
+  // the LDS address is wave-uniform too (free when it already sits in a
+  // scalar register)
+  const uint32_t lds_u = uint32_t(__builtin_amdgcn_readfirstlane(lds));
   // m0 is reserved to the compiler: saved and restored inside the asm
   uint32_t saved;
   asm volatile(
@@ -160,7 +163,7 @@ __device__ __forceinline__ void dma16(const char *base_in, int32_t voff, uint32_
       "s_nop 0\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "s"(lds), "v"(voff), "s"(base)
+      : "s"(lds_u), "v"(voff), "s"(base)
       : "memory");
 }
 
@@ -213,6 +216,7 @@ __device__ __forceinline__ void swap_halves(uint32_t &lo, uint32_t &hi) {
 struct TileCoord {
   int e, row0, prow0, m0, rows_valid, n0, cols_valid, k0, nk, grp;
   int p, N;  // problem (0: the main one, 1 / 2: wp[0] / wp[1]) and its columns
+  int mt;    // entry of the tile list (the forward's single-launch form)
 };
 
 template <int BM, int BN>
@@ -268,12 +272,81 @@ __device__ __forceinline__ void decode_tile_wg(const GemmArgs &g, int u, int per
   t.N = N;
 }
 
+// Byte size of the LDS ring of a 256 x BN tile (kStages stages of A and B
+// slices).
+template <int BN>
+constexpr uint32_t ring_bytes() {
+  return uint32_t(kStages) * (256 * kSK * 2 + BN * kSK * 2);
+}
+
+// Tile hand-out of a persistent launch, as the tile loop below sees it:
+//   request()  thread 0, at the start of every tile: ask for the next tile
+//              (e.g. from a counter) while the current one computes;
+//   next(t)    all threads, after the tile's main loop and its closing
+//              barrier: true with t the next tile of this loop (its first
+//              slices are requested during the epilogue), false when this
+//              loop ends after the current tile;
+//   done(c)    all threads, after tile c's epilogue (its stores issued);
+//   kCoherentC whether C is stored device-coherent (read by other tiles of
+//              the same launch).
+//
+// LaunchSched serves a launch of one problem: tiles (it * G + slot) of the
+// tile order, or, in the backward's multi-problem launch, the weight-gradient
+// tiles and then the main problem's tiles from the work counter g.queue (the
+// first G implicitly: tile blockIdx-derived slot).
+template <int BM, int BN, bool kMulti>
+struct LaunchSched {
+  static constexpr bool kCoherentC = false;  // C is read only by later launches
+  GemmArgs g;  // a copy (no reference to the kernel argument: its fields
+               // then stay in registers)
+  int n_mt, n_nt, per0, per1, n_wgt, G, slot, it;
+  int32_t *s_next;  // LDS: the next tile from the counter (multi-problem launch)
+
+  __device__ __forceinline__ LaunchSched(const GemmArgs g_, int32_t *s_next_) : g(g_), s_next(s_next_) {
+    n_mt = *g.n_mtiles;
+    n_nt = (g.N + BN - 1) / BN;
+    per0 = per1 = n_wgt = 0;
+    if constexpr (kMulti) {
+      per0 = ((g.wp[0].M + BM - 1) / BM) * ((g.wp[0].N + BN - 1) / BN);
+      per1 = ((g.wp[1].M + BM - 1) / BM) * ((g.wp[1].N + BN - 1) / BN);
+      n_wgt = *g.n_wg * (per0 + per1);
+    }
+    G = gridDim.x;  // a multiple of 8
+    // the hardware deals workgroups round-robin over the 8 XCDs: slot gives
+    // each XCD a contiguous block of G / 8 tiles of every round
+    slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
+    it = 0;
+  }
+  __device__ __forceinline__ bool decode(int u, TileCoord &c) const {
+    if (kMulti && u < n_wgt) {
+      decode_tile_wg<BM, BN>(g, u, per0, per1, c);
+      return true;
+    }
+    return decode_tile<BM, BN>(g, u - n_wgt, n_mt, n_nt, c);
+  }
+  __device__ __forceinline__ bool first(TileCoord &t) { return decode(slot, t); }
+  __device__ __forceinline__ void request() {
+    if (kMulti && threadIdx.x == 0) *s_next = atomicAdd(g.queue, 1) + G;
+  }
+  __device__ __forceinline__ bool next(TileCoord &t) {
+    ++it;
+    // (the value every thread reads from LDS is the same: stated, so the
+    // tile's coordinates stay in scalar registers)
+    return decode(kMulti ? __builtin_amdgcn_readfirstlane(*s_next) : it * G + slot, t);
+  }
+  __device__ __forceinline__ void done(const TileCoord &) {}
+};
+
 // A is row-major (lda) or, with kABlocked, in 16 x 32 blocks over padded
 // rows; C likewise with kCBlocked. B is always in 16 x 32 blocks.
-template <int BN, int WAVES_M, int WAVES_N, int kEpi, bool kABlocked, bool kCBlocked>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
-__attribute__((amdgpu_waves_per_eu(WAVES_M * WAVES_N / 4, WAVES_M * WAVES_N / 4)))
-void gemm256_kernel(GemmArgs g) {
+//
+// The tile loop of one workgroup: tiles from `sched`, starting with t (none
+// of whose slices has been requested yet), through the LDS ring at `smem`
+// (ring_bytes<BN>() bytes, 1 KB aligned).
+template <int BN, int WAVES_M, int WAVES_N, int kEpi, bool kABlocked, bool kCBlocked,
+          class Sched>
+__device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoord t,
+                                           Sched &sched) {
   constexpr int BM = 256;
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
@@ -301,7 +374,7 @@ void gemm256_kernel(GemmArgs g) {
   // stage s: A rows at s * STAGE_BYTES, then B rows; the last two stages are
   // also the epilogue's staging area
   constexpr uint32_t STAGE_BYTES = A_STAGE_BYTES + B_STAGE_BYTES;
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE_BYTES];
+  static_assert(kStages * STAGE_BYTES == ring_bytes<BN>(), "ring size");
   auto stageA = [&](int st) { return reinterpret_cast<const uint16_t *>(smem + st * STAGE_BYTES); };
   auto stageB = [&](int st) {
     return reinterpret_cast<const uint16_t *>(smem + st * STAGE_BYTES + A_STAGE_BYTES);
@@ -310,36 +383,21 @@ void gemm256_kernel(GemmArgs g) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const int n_mt = *g.n_mtiles;
-  const int n_nt = (g.N + BN - 1) / BN;
-  int per0 = 0, per1 = 0, n_wgt = 0;
-  if constexpr (kMulti) {
-    per0 = ((g.wp[0].M + BM - 1) / BM) * ((g.wp[0].N + BN - 1) / BN);
-    per1 = ((g.wp[1].M + BM - 1) / BM) * ((g.wp[1].N + BN - 1) / BN);
-    n_wgt = *g.n_wg * (per0 + per1);
-  }
-  const int G = gridDim.x;  // a multiple of 8
-  const int slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
-  auto decode = [&](int u, TileCoord &c) {
-    if (kMulti && u < n_wgt) {
-      decode_tile_wg<BM, BN>(g, u, per0, per1, c);
-      return true;
-    }
-    return decode_tile<BM, BN>(g, u - n_wgt, n_mt, n_nt, c);
-  };
-  __shared__ int32_t s_next;  // multi-problem launch: the next tile from the counter
-  const int kc_load = (lane & 3) ^ ((lane >> 4) & 3);
   const int64_t lda_b = g.lda * 2;
-  // a 16 x 32 block is 1 KB; lane l fills LDS bytes 16l .. 16l+15 = row
-  // l / 4, chunk slot l % 4, which holds logical chunk kc_load of that row
-  const int32_t blk_lane = (lane >> 2) * 64 + kc_load * 16;
   const uint32_t sA0 = lds_addr(smem), sB0 = sA0 + A_STAGE_BYTES;
 
-  TileCoord t;
-  if (!decode(slot, t)) return;
   const char *Ab, *Bb;
   int32_t offA[A_PER_WAVE], offB[B_SLOTS];
   auto setup = [&](const TileCoord &c) {
+    // The lane-derived parts are recomputed for every tile from a lane index
+    // the compiler cannot hoist out of the tile loop, so they occupy no
+    // register across it. A 16 x 32 block is 1 KB; lane l fills LDS bytes
+    // 16l .. 16l+15 = row l / 4, chunk slot l % 4, which holds logical
+    // chunk kc_load of that row.
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int kc_load = (ln & 3) ^ ((ln >> 4) & 3);
+    const int32_t blk_lane = (ln >> 2) * 64 + kc_load * 16;
     const uint16_t *Ap = g.A, *Bp = g.B;
     int64_t a_bs = g.a_blk_stride, b_es = g.b_expert_stride, b_bs = g.b_blk_stride;
     if (kMulti && c.p != 0) {
@@ -363,10 +421,13 @@ void gemm256_kernel(GemmArgs g) {
       }
     } else {
       Ab = reinterpret_cast<const char *>(g.A) + int64_t(c.row0 + c.m0) * lda_b;
+      // 24-bit operands (r < 256, lda_b <= 2 * LLEP_MAX_FFN_DIM bytes): one
+      // multiply-add with a 32-bit addend per offset
+      const uint32_t lda_b32 = uint32_t(lda_b);
 #pragma unroll
       for (int j = 0; j < A_PER_WAVE; ++j) {
-        const int r = min((wave + NWD * j) * 16 + (lane >> 2), c.rows_valid - 1);
-        offA[j] = int32_t(r * lda_b + kc_load * 16);
+        const int r = min((wave + NWD * j) * 16 + (ln >> 2), c.rows_valid - 1);
+        offA[j] = int32_t(__umul24(uint32_t(r), lda_b32) + uint32_t(kc_load * 16));
       }
     }
     Bb = reinterpret_cast<const char *>(Bp) + int64_t(c.e) * b_es * 2 + (c.n0 >> 4) * b_bs +
@@ -478,11 +539,11 @@ void gemm256_kernel(GemmArgs g) {
     }
   };
 
-  for (int it = 0;; ++it) {
+  for (;;) {
     const int nk = t.nk;
-    // the tile after this one (read after the barrier that ends the loop;
-    // rewritten only after the barrier that ends the epilogue)
-    if (kMulti && threadIdx.x == 0) s_next = atomicAdd(g.queue, 1) + G;
+    // ask for the tile after this one (read after the barrier that ends the
+    // loop; rewritten only after the barrier that ends the epilogue)
+    sched.request();
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -577,7 +638,7 @@ void gemm256_kernel(GemmArgs g) {
     // every wave is done with the ring before the next tile's slices land
     __syncthreads();
     const TileCoord c = t;
-    const bool more = decode(kMulti ? s_next : (it + 1) * G + slot, t);
+    const bool more = sched.next(t);
     // the next tile's first kAhead - 1 slices load during the epilogue; the
     // last stages hold the epilogue's staging area until the barrier below
     static_assert(kStages - (kAhead - 1) >= 2, "two stages free for staging");
@@ -664,9 +725,28 @@ void gemm256_kernel(GemmArgs g) {
 #pragma unroll
         for (int rb = 0; rb < WM / 16; ++rb) {
           if (rb * 16 >= rows_w) break;  // the group's padded rows end here
-          *reinterpret_cast<i32x4 *>(dst + int64_t(rb) * (g.ldc >> 5) * 1024) =
-              *reinterpret_cast<const i32x4 *>(
-              sp + rb * 1024 + (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) << 4));
+          char *d = dst + int64_t(rb) * (g.ldc >> 5) * 1024;
+          if constexpr (Sched::kCoherentC) {
+            // device-coherent stores (written through the XCD's L2), so a
+            // reader on another XCD in the same launch finds them in memory
+            // once they have completed: 8 bytes per lane, lane l at bytes
+            // 8 l of each half of the block, so each store instruction
+            // writes 512 contiguous bytes (whole lines)
+            char *blk0 = reinterpret_cast<char *>(d - lane * 16);
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+              const int o = half * 512 + lane * 8;  // byte of the block
+              const int row = o >> 6, chunk = (o >> 4) & 3;
+              const uint2 v = *reinterpret_cast<const uint2 *>(
+                  sp + rb * 1024 + row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4) + (o & 8));
+              __hip_atomic_store(reinterpret_cast<uint64_t *>(blk0 + o),
+                                 uint64_t(v.x) | (uint64_t(v.y) << 32), __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+            }
+          } else {
+            *reinterpret_cast<i32x4 *>(d) = *reinterpret_cast<const i32x4 *>(
+                sp + rb * 1024 + (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) << 4));
+          }
         }
       }
     } else if constexpr (kEpi == kEpiSwigluBwd) {
@@ -894,6 +974,7 @@ void gemm256_kernel(GemmArgs g) {
         rowmajor_epilogue();
       }
     }
+    sched.done(c);
     if (more) {
       // the staging area is the last stages of the ring again: every wave's
       // staging reads are done (lgkmcnt) before slice kAhead - 1 may land
@@ -903,6 +984,20 @@ void gemm256_kernel(GemmArgs g) {
     }
     if (!more) break;
   }
+}
+
+// One persistent launch of one problem (forward projections, backward
+// GEMMs): one workgroup per CU walks its tiles (LaunchSched).
+template <int BN, int WAVES_M, int WAVES_N, int kEpi, bool kABlocked, bool kCBlocked>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
+__attribute__((amdgpu_waves_per_eu(WAVES_M * WAVES_N / 4, WAVES_M * WAVES_N / 4)))
+void gemm256_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) char smem[ring_bytes<BN>()];
+  __shared__ int32_t s_next;  // multi-problem launch: the next tile from the counter
+  LaunchSched<256, BN, kEpi == kEpiBwdMulti> sched(g, &s_next);
+  TileCoord t;
+  if (!sched.first(t)) return;
+  gemm_tiles<BN, WAVES_M, WAVES_N, kEpi, kABlocked, kCBlocked>(g, smem, t, sched);
 }
 
 // ---------------------------------------------------------------------------

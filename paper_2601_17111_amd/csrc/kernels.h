@@ -72,6 +72,7 @@ struct FfnArgs {
   void *gate_up_out;  // training forward: raw gate / up values per x_perm row; null: none
   void *ws;
   size_t ws_bytes;
+  int32_t *status;  // the plan's status word (LLEP_STATUS_FFN_WAIT)
 };
 size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t F,
                            llep_dtype dtype);

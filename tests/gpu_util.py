@@ -117,6 +117,9 @@ class LayerRun:
 
     def forward(self, device=-1):
         import torch
+        from paper_2601_17111_amd import binding as B
         self.layer.forward(self.ids, self.gates, self.x, self.gu, self.dn, device)
         torch.cuda.synchronize()
+        # no down-projection tile gave up waiting for its activations
+        assert not self.layer.bufs.info_dict()["status"] & B.LLEP_STATUS_FFN_WAIT
         return self.layer.y

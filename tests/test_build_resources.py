@@ -1,6 +1,8 @@
 """Compiler resource checks on the gfx950 code objects (CPU only: hipcc
 cross-compiles). Every kernel must build without scratch memory or VGPR
-spills, and fit the 160 KiB of LDS of a compute unit."""
+spills, and fit the 160 KiB of LDS of a compute unit; and no inline asm may
+rely on a clobber of a register the compiler reserves (m0: such a clobber is
+not honoured, so a value the compiler keeps there would be overwritten)."""
 
 import os
 import re
@@ -23,6 +25,7 @@ def _resources(src, tmp_path):
            "-Rpass-analysis=kernel-resource-usage"]
     p = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     assert p.returncode == 0, p.stdout
+    assert "clobber list contains reserved registers" not in p.stdout, p.stdout
     kernels, cur = {}, None
     for line in p.stdout.splitlines():
         m = re.search(r"remark:\s+Function Name: (\S+)", line)

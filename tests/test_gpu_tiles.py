@@ -123,3 +123,42 @@ def test_a1_same_work_over_more_experts(dev, N):
         got_all.append(got)
         want_all.append(want)
     report(cfg.name, np.concatenate(got_all), np.concatenate(want_all))
+
+
+@pytest.mark.parametrize("D,F", [(2880, 2880), (2048, 768), (256, 320)],
+                         ids=["down192", "down256", "small"])
+def test_single_launch_waits_repeatable(dev, D, F):
+    """Both projections run in one launch; a down-projection tile waits for
+    the gate/up tiles of its rows, which may run on other XCDs. On a layer
+    small enough that most workgroups start out waiting, twenty calls give
+    the same bits, the LLEP and EP plans give the same bits per row, no wait
+    gives up (status), and sampled rows match the oracle."""
+    import torch
+    from paper_2601_17111_amd import binding as B
+    from paper_2601_17111_amd.synth import LayerConfig
+    cfg = LayerConfig(f"wait-D{D}-F{F}", T=700, D=D, F=F, E=16, K=4, P=4,
+                      alpha=Fraction(11, 10), dtype="bf16", routing=("hot", 0.8, 1))
+    run = LayerRun(cfg, 2, dev)
+    L = run.layer
+    y0 = run.forward(-1).clone()
+    out0 = L.out_perm.clone()
+    for _ in range(20):
+        L.ffn(run.gu, run.dn, -1)
+        torch.cuda.synchronize()
+        assert torch.equal(L.out_perm, out0)
+    assert not L.bufs.info_dict()["status"] & B.LLEP_STATUS_FFN_WAIT
+    L.set_mode("ep")
+    assert torch.equal(run.forward(-1), y0)
+    L.set_mode("llep")
+    run.forward(-1)
+    info = L.bufs.info_dict()
+    n = info["total_rows"]
+    rows = np.linspace(0, n - 1, 16).astype(int)
+    row_pair = L.row_pair[:n].cpu().numpy()
+    ids = run.inp.ids.reshape(-1)
+    W = run.host_weights(range(cfg.E))
+    got = L.out_perm[torch.from_numpy(rows).to(dev)].float().cpu().numpy()
+    for i, r in enumerate(rows):
+        p = int(row_pair[r])
+        want = oracle.swiglu_ffn(run.inp.x[p // cfg.K][None], *_w64(W, int(ids[p])))[0]
+        assert rel_err(got[i], want) <= TOL_BF16
