@@ -87,7 +87,8 @@ int32_t llep_plan_max_chunks(const llep_plan_params *params) {
 int64_t llep_plan_rank_base_elems(const llep_plan_params *params) {
   if (check_params(params) != LLEP_OK) return -1;
   const int64_t tiles = llep::rank_tiles(params->T * params->K);
-  return tiles * params->E + tiles;
+  // per tile: E counts (then bases), a bad-id flag, E counts per slice
+  return tiles * params->E + tiles + tiles * llep::kRankWaves * params->E;
 }
 
 int llep_plan(const llep_plan_params *params, const int32_t *topk_ids,

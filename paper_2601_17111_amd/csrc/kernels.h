@@ -14,10 +14,11 @@ constexpr int kMaxChunks = 2 * LLEP_MAX_EXPERTS + LLEP_MAX_DEVICES;
 // count is bounded by 2E + P).
 constexpr int32_t kStatusPlanOverflow = 1 << 30;
 
-// Pairs are counted and ranked in tiles of kRankTile pairs (one workgroup
-// each); each of the kRankWaves waves of a tile owns a contiguous
-// kRankSub-pair slice of it. rank_base holds one row of E counts (then
-// exclusive bases) per tile.
+// Pairs are counted in tiles of kRankTile pairs (one workgroup each), and
+// per slice of kRankSub pairs (a wave's share of a tile); they are ranked
+// slice by slice (one workgroup per slice, 64 pairs per wave). rank_base
+// holds one row of E counts (then exclusive bases) per tile, a bad-id flag
+// per tile, and a row of E counts per slice.
 constexpr int kRankTile = 1024;
 constexpr int kRankWaves = 4;
 constexpr int kRankSub = kRankTile / kRankWaves;

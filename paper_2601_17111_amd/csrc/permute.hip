@@ -5,13 +5,15 @@
 // chunk (d, e, s, t) of the plan with s <= r < t, and goes to row
 // chunk_row + (r - s).
 //
-// rank_kernel    one workgroup per rank tile of kRankTile pairs. The tile's
-//                base rank per expert comes from the plan's scan of the
-//                histogram; inside the tile each wave owns a contiguous slice
-//                and ranks its pairs with ballot-built match masks, so the
-//                order never depends on atomics. The chunk table is copied
-//                to LDS first, so finding a pair's chunk reads no memory.
-//                Writes pair_row, row_pair and gate_perm.
+// rank_kernel    one workgroup per slice of kRankSub pairs (a quarter of a
+//                histogram tile). The slice's base rank per expert is its
+//                tile's base (the plan's scan of the histogram) plus the
+//                histogram's counts of the tile's earlier slices; inside the
+//                slice each wave owns 64 consecutive pairs and ranks them
+//                with ballot-built match masks, so the order never depends
+//                on atomics. The chunk table is copied to LDS first, so
+//                finding a pair's chunk reads no memory. Writes pair_row,
+//                row_pair and gate_perm.
 // gather_kernel  one wavefront per token: reads x[t] once (16-byte vectors)
 //                and writes it to the K rows of the token's pairs.
 #include "common.h"
@@ -21,7 +23,7 @@ namespace llep {
 
 __global__ __launch_bounds__(256) void rank_kernel(
     const int32_t *__restrict__ ids, const float *__restrict__ gates, int64_t R,
-    int32_t E, int32_t max_chunks, const int32_t *__restrict__ rank_base,
+    int32_t E, int32_t max_chunks, int32_t n_tiles, const int32_t *__restrict__ rank_base,
     const int32_t *__restrict__ chunks, const int32_t *__restrict__ chunk_row,
     const int32_t *__restrict__ expert_chunk_begin, int32_t *__restrict__ pair_row,
     int32_t *__restrict__ row_pair, float *__restrict__ gate_perm) {
@@ -36,32 +38,35 @@ __global__ __launch_bounds__(256) void rank_kernel(
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int nb = bits_for(uint32_t(E));
-  const int64_t tile0 = int64_t(blockIdx.x) * kRankTile;
-  const int64_t s0 = tile0 + int64_t(w) * kRankSub;
-  // Every global load is issued up front (the wave's ids and gates, kept in
-  // registers for both passes; the tile's base row; the chunk table), so
-  // the kernel waits on memory once instead of once per step.
-  static_assert(kRankWaves * kWave == 256, "one rank tile per 256-thread workgroup");
-  constexpr int kIter = kRankSub / kWave;
-  constexpr int kBaseIter = (LLEP_MAX_EXPERTS + 255) / 256;
-  uint32_t ev[kIter];
-  float gv[kIter];
-#pragma unroll
-  for (int j = 0; j < kIter; ++j) {
-    const int64_t p = s0 + j * kWave + lane_id();
-    int32_t v = E;  // sentinel: past the end or invalid
-    gv[j] = 0.0f;
-    if (p < R) {
-      v = ids[p];
-      gv[j] = gates[p];
-    }
-    ev[j] = v >= 0 && v < E ? uint32_t(v) : uint32_t(E);
+  // slice blockIdx.x = slice `sub` of rank tile `tile`; wave w ranks its 64
+  // consecutive pairs
+  const int64_t tile = blockIdx.x / kRankWaves;
+  const int sub = int(blockIdx.x % kRankWaves);
+  const int64_t p = int64_t(blockIdx.x) * kRankSub + w * kWave + lane_id();
+  static_assert(kRankSub == kRankWaves * kWave, "a slice is one 64-pair block per wave");
+  // Every global load is issued up front (the pair's id and gate, the
+  // slice's base ranks, the chunk table), so the kernel waits on memory once.
+  uint32_t ev = uint32_t(E);  // sentinel: past the end or invalid
+  float gv = 0.0f;
+  if (p < R) {
+    const int32_t v = ids[p];
+    gv = gates[p];
+    if (v >= 0 && v < E) ev = uint32_t(v);
   }
-  int32_t rbv[kBaseIter];
+  // base rank of each expert in this slice: the tile's base (the plan's
+  // scan of the tile counts) plus the counts of the tile's earlier slices
+  constexpr int kBaseIter = (LLEP_MAX_EXPERTS + 255) / 256;
+  const int32_t *slice_cnt = rank_base + int64_t(n_tiles) * (E + 1) + tile * kRankWaves * E;
+  int32_t sb[kBaseIter];
 #pragma unroll
   for (int i = 0; i < kBaseIter; ++i) {
     const int e = tid + 256 * i;
-    rbv[i] = e < E ? rank_base[int64_t(blockIdx.x) * E + e] : 0;
+    int32_t b = 0;
+    if (e < E) {
+      b = rank_base[tile * E + e];
+      for (int v = 0; v < sub; ++v) b += slice_cnt[v * E + e];
+    }
+    sb[i] = b;
   }
   const int nc = min(max(expert_chunk_begin[E], 0), min(max_chunks, kMaxChunks));
   for (int i = tid; i < kRankWaves * E; i += blockDim.x) wbase[i] = 0;
@@ -72,21 +77,16 @@ __global__ __launch_bounds__(256) void rank_kernel(
     c_row[c] = chunk_row[c];
   }
   __syncthreads();
-
-  // pass A: per-wave counts of each expert in the wave's slice
-#pragma unroll
-  for (int j = 0; j < kIter; ++j) {
-    const uint32_t e = ev[j];
-    const uint64_t m = match_any(e, nb);
-    if (e < uint32_t(E) && (m & lanemask_lt()) == 0) wbase[w * E + e] += __popcll(m);
-  }
+  // per-wave counts of each expert (one leader lane per expert value)
+  const uint64_t m = match_any(ev, nb);
+  if (ev < uint32_t(E) && (m & lanemask_lt()) == 0) wbase[w * E + ev] = __popcll(m);
   __syncthreads();
-  // wave bases = tile base + counts of the earlier waves of the tile
+  // wave bases = slice base + counts of the slice's earlier waves
 #pragma unroll
   for (int i = 0; i < kBaseIter; ++i) {
     const int e = tid + 256 * i;
     if (e >= E) continue;
-    int32_t run = rbv[i];
+    int32_t run = sb[i];
     for (int v = 0; v < kRankWaves; ++v) {
       const int32_t c = wbase[v * E + e];
       wbase[v * E + e] = run;
@@ -94,33 +94,23 @@ __global__ __launch_bounds__(256) void rank_kernel(
     }
   }
   __syncthreads();
-
-  // pass B: rank, locate the chunk, write the row
-#pragma unroll
-  for (int j = 0; j < kIter; ++j) {
-    const int64_t p = s0 + j * kWave + lane_id();
-    const uint32_t e = ev[j];
-    const uint64_t m = match_any(e, nb);
-    int32_t r = 0;
-    if (e < uint32_t(E)) r = wbase[w * E + e] + __popcll(m & lanemask_lt());
-    __builtin_amdgcn_wave_barrier();
-    if (e < uint32_t(E) && (m & lanemask_lt()) == 0) wbase[w * E + e] += __popcll(m);
-    if (e < uint32_t(E)) {
-      int c = ecb[e];
-      const int c1 = max(ecb[e + 1], c);
-      while (c + 1 < c1 && r >= c_end[c]) ++c;
-      // a pair outside every chunk of its expert (a plan built from other
-      // ids) gets no row
-      const bool inside = c < c1 && r >= c_start[c] && r < c_end[c];
-      const int32_t row = inside ? c_row[c] + (r - c_start[c]) : -1;
-      pair_row[p] = row;
-      if (row >= 0 && row < R) {
-        row_pair[row] = int32_t(p);
-        gate_perm[row] = gv[j];
-      }
-    } else if (p < R) {
-      pair_row[p] = -1;
+  // rank, locate the chunk, write the row
+  if (ev < uint32_t(E)) {
+    const int32_t r = wbase[w * E + ev] + __popcll(m & lanemask_lt());
+    int c = ecb[ev];
+    const int c1 = max(ecb[ev + 1], c);
+    while (c + 1 < c1 && r >= c_end[c]) ++c;
+    // a pair outside every chunk of its expert (a plan built from other
+    // ids) gets no row
+    const bool inside = c < c1 && r >= c_start[c] && r < c_end[c];
+    const int32_t row = inside ? c_row[c] + (r - c_start[c]) : -1;
+    pair_row[p] = row;
+    if (row >= 0 && row < R) {
+      row_pair[row] = int32_t(p);
+      gate_perm[row] = gv;
     }
+  } else if (p < R) {
+    pair_row[p] = -1;
   }
 }
 
@@ -222,9 +212,11 @@ void launch_gather_v(int grid, hipStream_t stream, const PermuteArgs &a, int32_t
 hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
   if (a.R == 0) return hipSuccess;
   const size_t lds = (size_t(kRankWaves + 1) * a.E + 1 + 3 * size_t(kMaxChunks)) * sizeof(int32_t);
-  hipLaunchKernelGGL(rank_kernel, dim3(a.n_tiles), dim3(256), lds, stream, a.ids, a.gates,
-                     a.R, a.E, a.max_chunks, a.plan.rank_base, a.plan.chunks, a.plan.chunk_row,
-                     a.plan.expert_chunk_begin, a.pair_row, a.row_pair, a.gate_perm);
+  const int64_t slices = (a.R + kRankSub - 1) / kRankSub;
+  hipLaunchKernelGGL(rank_kernel, dim3(slices), dim3(256), lds, stream, a.ids, a.gates,
+                     a.R, a.E, a.max_chunks, a.n_tiles, a.plan.rank_base, a.plan.chunks,
+                     a.plan.chunk_row, a.plan.expert_chunk_begin, a.pair_row, a.row_pair,
+                     a.gate_perm);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int32_t vecs = int32_t((int64_t(a.D) * a.elem_bytes) / 16);

@@ -1,7 +1,8 @@
 // Steps 1-2 of the LLEP hot path: the routing histogram and the plan.
 //
-// hist_kernel   counts, per rank tile of kRankTile pairs, how many pairs go
-//               to each expert (Alg. 4, first step: the global per-expert loads).
+// hist_kernel   counts, per rank tile of kRankTile pairs and per slice of
+//               kRankSub pairs, how many pairs go to each expert (Alg. 4,
+//               first step: the global per-expert loads).
 // plan_kernel   one workgroup: scans the tile counts into per-tile rank bases
 //               and the loads l, runs the lambda test (Alg. 4), then the
 //               least-loaded assignment (Alg. 2 with the spill loop of
@@ -25,18 +26,22 @@ int64_t rank_tiles(int64_t R) { return (R + kRankTile - 1) / kRankTile; }
 // histogram
 // ---------------------------------------------------------------------------
 
-// rank_base layout: [n_tiles][E] counts, then [n_tiles] bad-id flags.
+// rank_base layout: [n_tiles][E] counts (the plan turns them into each
+// tile's base ranks), then [n_tiles] bad-id flags, then [n_tiles][kRankWaves][E]
+// counts of each kRankSub-pair slice of a tile (a wave's share here; the
+// permutation ranks slice by slice from them).
 __global__ __launch_bounds__(256) void hist_kernel(const int32_t *__restrict__ ids,
                                                    int64_t R, int32_t E,
                                                    int32_t n_tiles,
                                                    int32_t *__restrict__ rank_base) {
-  extern __shared__ int32_t cnt[];  // [E]
+  extern __shared__ int32_t cnt[];  // [kRankWaves][E]
   const int tid = threadIdx.x;
-  for (int i = tid; i < E; i += blockDim.x) cnt[i] = 0;
+  for (int i = tid; i < kRankWaves * E; i += blockDim.x) cnt[i] = 0;
   __syncthreads();
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int nb = bits_for(uint32_t(E));
   const int64_t s0 = int64_t(blockIdx.x) * kRankTile + int64_t(w) * kRankSub;
+  int32_t *wcnt = cnt + w * E;
   int bad = 0;
   for (int j = 0; j < kRankSub; j += kWave) {
     if (s0 + j >= R) break;  // uniform in the wave
@@ -48,12 +53,22 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t *__restrict__ i
       else bad = 1;
     }
     const uint64_t m = match_any(e, nb);
-    if (e < uint32_t(E) && (m & lanemask_lt()) == 0)
-      atomicAdd(&cnt[e], __popcll(m));
+    // one leader lane per expert value: no two lanes add to the same count
+    if (e < uint32_t(E) && (m & lanemask_lt()) == 0) wcnt[e] += __popcll(m);
   }
   bad = __syncthreads_or(bad);
   int32_t *row = rank_base + int64_t(blockIdx.x) * E;
-  for (int i = tid; i < E; i += blockDim.x) row[i] = cnt[i];
+  int32_t *slices = rank_base + int64_t(n_tiles) * (E + 1) + int64_t(blockIdx.x) * kRankWaves * E;
+  for (int i = tid; i < E; i += blockDim.x) {
+    int32_t tot = 0;
+#pragma unroll
+    for (int v = 0; v < kRankWaves; ++v) {
+      const int32_t c = cnt[v * E + i];
+      slices[v * E + i] = c;
+      tot += c;
+    }
+    row[i] = tot;
+  }
   if (tid == 0) rank_base[int64_t(n_tiles) * E + blockIdx.x] = bad;
 }
 
@@ -475,7 +490,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
   if (a.n_tiles > 0) {
     hipLaunchKernelGGL(hist_kernel, dim3(a.n_tiles), dim3(256),
-                       size_t(a.E) * sizeof(int32_t), stream, a.ids, a.R, a.E,
+                       size_t(kRankWaves) * a.E * sizeof(int32_t), stream, a.ids, a.R, a.E,
                        a.n_tiles, a.buf.rank_base);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;

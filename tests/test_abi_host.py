@@ -56,9 +56,10 @@ def test_size_queries():
     p = _params()
     assert B.llep_plan_max_chunks(p) == 2 * 8 + 4
     tiles = -(-256 * 2 // 1024)  # pairs are ranked in tiles of 1024
-    assert B.llep_plan_rank_base_elems(p) == tiles * 8 + tiles
+    # per tile: E counts (then bases), a bad-id flag, E counts per 256-pair slice
+    assert B.llep_plan_rank_base_elems(p) == tiles * 8 + tiles + tiles * 4 * 8
     p = _params(T=65536, K=8, E=128, P=8, capacity=72090)
-    assert B.llep_plan_rank_base_elems(p) == 512 * 128 + 512
+    assert B.llep_plan_rank_base_elems(p) == 512 * 128 + 512 + 512 * 4 * 128
     ws = B.llep_grouped_ffn_workspace_bytes(p, 768, B.LLEP_BF16)
     assert ws >= 65536 * 8 * 768 * 2
     L = B.lib()
