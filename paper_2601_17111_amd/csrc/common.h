@@ -43,11 +43,22 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(uint32_t(h) << 16);
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> a packed bfloat16 pair (lo in bits 0..15), rounded to
+// nearest even (NaN stays NaN) by the gfx950 pair conversion
+// (v_cvt_pk_bf16_f32: one instruction, no branch). For every input that is
+// not a NaN it gives the bits of the rounding formula
+// (u + 0x7fff + ((u >> 16) & 1)) >> 16 on the float's bits u.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
 // float -> bfloat16, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-  return uint16_t((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+  return uint16_t(pack_bf16x2(f, 0.0f));
 }
 
 }  // namespace llep

@@ -660,9 +660,7 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
     char *stg = smem + (kStages - 2) * STAGE_BYTES + wave * STAGING;
     const int rows_w = c.rows_valid - wm * WM;  // valid rows of this wave's tile part
     const int h = lane >> 5;
-    auto pack2 = [](float lo, float hi) {
-      return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
-    };
+    auto pack2 = [](float lo, float hi) { return pack_bf16x2(lo, hi); };
     if constexpr (kSwiglu) {
       // gate columns 64p .. 64p+31 and the matching up columns 64p+32 ..
       // 64p+63 of the tile give activation columns f = 32 (pc / 64) + 0..31.

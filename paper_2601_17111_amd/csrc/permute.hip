@@ -322,8 +322,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const i32x4 *__restrict__ 
           if (kBf16) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              q[i] = int32_t(uint32_t(f32_to_bf16(acc[b][2 * i])) |
-                             (uint32_t(f32_to_bf16(acc[b][2 * i + 1])) << 16));
+              q[i] = int32_t(pack_bf16x2(acc[b][2 * i], acc[b][2 * i + 1]));
           } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i) q[i] = __float_as_int(acc[b][i]);
@@ -439,8 +438,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(
                   const float d0 = __uint_as_float(du << 16), d1 = __uint_as_float(du & 0xffff0000u);
                   part = fmaf(d0, __uint_as_float(qu << 16), part);
                   part = fmaf(d1, __uint_as_float(qu & 0xffff0000u), part);
-                  o[i] = int32_t(uint32_t(f32_to_bf16(g[j] * d0)) |
-                                 (uint32_t(f32_to_bf16(g[j] * d1)) << 16));
+                  o[i] = int32_t(pack_bf16x2(g[j] * d0, g[j] * d1));
                 } else {
                   const float d0 = __int_as_float(dv[b][i]);
                   part = fmaf(d0, __int_as_float(q[j][b][i]), part);
