@@ -906,28 +906,44 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
         float *C2 = g.wp[0].C2;
         const bool gate_up = !second && g.wp[0].gate_up;
         const int64_t es = second ? g.wp[1].expert_stride : g.wp[0].expert_stride;
+        // The fp32 gradients leave as whole 128-byte row pieces: each 32 x 32
+        // block is written to the wave's staging area (rows RSF bytes apart,
+        // so the 32 rows of a write spread over the banks) and read back so
+        // that store k covers rows 8k .. 8k+7 of the block, lane l row
+        // 8k + l / 8 and columns 4 (l % 8) .. 4 (l % 8) + 3. (Stored straight
+        // from the accumulators, every store instruction wrote 32-byte pieces
+        // of 32 rows, and the many short tiles of the small experts were
+        // bound by those partial-line writes.)
+        constexpr int RSF = 32 * 4 + 16;
+        static_assert(32 * RSF <= STAGING, "staging");
+        const int ld = gate_up ? (c.N >> 1) : c.N;  // fp32 elements per gradient row
+        const int rr = lane >> 3, rc = (lane & 7) * 4;  // read-back row / column of the lane
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-          const int m = c.m0 + wm * WM + i * 32 + (lane & 31);
           if (i * 32 >= rows_w) break;
-          if (i * 32 + (lane & 31) >= rows_w) continue;
+          const int m0 = c.m0 + wm * WM + i * 32;  // first gradient row of the block
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int col0 = c.n0 + wn * WN + j * 32;
             if (col0 >= c.N) continue;
+            // gate / up columns are interleaved per 32 in the tile: the block
+            // belongs to one of the two gradients, at column 32 (col0 / 64)
+            float *base;
+            if (gate_up)
+              base = ((col0 & 32) ? C2 : C) + int64_t(c.e) * es + 32 * (col0 >> 6);
+            else
+              base = C + int64_t(c.e) * es + col0;
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-              const int n = col0 + 8 * gq + 4 * h;
-              float *dst;
-              if (gate_up) {
-                const int q = n >> 6, cc = n & 63;
-                dst = (cc < 32 ? C : C2) + int64_t(c.e) * es + int64_t(m) * (c.N >> 1) + 32 * q +
-                      (cc & 31);
-              } else {
-                dst = C + int64_t(c.e) * es + int64_t(m) * c.N + n;
-              }
-              *reinterpret_cast<f32x4 *>(dst) = f32x4{acc[i][j][4 * gq], acc[i][j][4 * gq + 1],
-                                                      acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]};
+            for (int gq = 0; gq < 4; ++gq)
+              *reinterpret_cast<f32x4 *>(stg + (lane & 31) * RSF + (8 * gq + 4 * h) * 4) =
+                  f32x4{acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2],
+                        acc[i][j][4 * gq + 3]};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const int r = 8 * k + rr;
+              const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + r * RSF + rc * 4);
+              if (i * 32 + r < rows_w)
+                *reinterpret_cast<f32x4 *>(base + int64_t(m0 + r) * ld + rc) = v;
             }
           }
         }
