@@ -99,11 +99,13 @@ struct GemmArgs {
   int64_t kmax;
   // multi-problem backward launch: weight-gradient tiles of the experts in
   // wg_experts (longest k-segment first), problem wp[0] then wp[1] per
-  // expert, then the tiles of the main problem; tiles past the first gridDim
-  // come from the counter *queue (zero before the launch)
+  // expert, and the tiles of the main problem, handed out longest first
+  // (LaunchSched::decode); tiles past the first gridDim come from the
+  // counter *queue (zero before the launch)
   WgProblem wp[2];
   const int4 *wg_experts;  // (expert, first k-slice, k-slices, 0)
   const int32_t *n_wg;
+  const int32_t *n_wg_long;  // the first of them whose tiles are at least as long as a main tile
   int32_t *queue;
 };
 
@@ -299,17 +301,18 @@ struct LaunchSched {
   static constexpr bool kCoherentC = false;  // C is read only by later launches
   GemmArgs g;  // a copy (no reference to the kernel argument: its fields
                // then stay in registers)
-  int n_mt, n_nt, per0, per1, n_wgt, G, slot, it;
+  int n_mt, n_nt, per0, per1, n_wgt, n_long, G, slot, it;
   int32_t *s_next;  // LDS: the next tile from the counter (multi-problem launch)
 
   __device__ __forceinline__ LaunchSched(const GemmArgs g_, int32_t *s_next_) : g(g_), s_next(s_next_) {
     n_mt = *g.n_mtiles;
     n_nt = (g.N + BN - 1) / BN;
-    per0 = per1 = n_wgt = 0;
+    per0 = per1 = n_wgt = n_long = 0;
     if constexpr (kMulti) {
       per0 = ((g.wp[0].M + BM - 1) / BM) * ((g.wp[0].N + BN - 1) / BN);
       per1 = ((g.wp[1].M + BM - 1) / BM) * ((g.wp[1].N + BN - 1) / BN);
       n_wgt = *g.n_wg * (per0 + per1);
+      n_long = *g.n_wg_long * (per0 + per1);
     }
     G = gridDim.x;  // a multiple of 8
     // the hardware deals workgroups round-robin over the 8 XCDs: slot gives
@@ -317,12 +320,21 @@ struct LaunchSched {
     slot = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
     it = 0;
   }
+  // The multi-problem launch hands its tiles out longest first, so that the
+  // last ones to start are short and the workgroups finish together: the
+  // weight-gradient tiles of the experts whose k-segment is at least as long
+  // as a main tile's, then the main tiles, then the other weight-gradient
+  // tiles.
   __device__ __forceinline__ bool decode(int u, TileCoord &c) const {
-    if (kMulti && u < n_wgt) {
-      decode_tile_wg<BM, BN>(g, u, per0, per1, c);
-      return true;
+    if constexpr (kMulti) {
+      const int n_main = n_mt * n_nt;
+      if (u < n_long || (u >= n_long + n_main && u < n_wgt + n_main)) {
+        decode_tile_wg<BM, BN>(g, u < n_long ? u : u - n_main, per0, per1, c);
+        return true;
+      }
+      return decode_tile<BM, BN>(g, u - n_long, n_mt, n_nt, c);
     }
-    return decode_tile<BM, BN>(g, u - n_wgt, n_mt, n_nt, c);
+    return decode_tile<BM, BN>(g, u, n_mt, n_nt, c);
   }
   __device__ __forceinline__ bool first(TileCoord &t) { return decode(slot, t); }
   __device__ __forceinline__ void request() {

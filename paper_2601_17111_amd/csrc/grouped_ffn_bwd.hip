@@ -39,7 +39,7 @@ static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t 
   L.max_mtiles = R / kTileM + L.max_groups + 1;
   L.prow_max = R + 16 * L.max_groups;
   L.kmax = (R + 32 * L.max_groups + 31) / 32 * 32;
-  size_t o = 256;  // counters: n_mtiles, n_wg, k-slices in use
+  size_t o = 256;  // counters: n_mtiles, n_wg, k-slices in use, work counter, long n_wg
   L.tiles_off = o;  o = round256(o + size_t(L.max_mtiles) * 16);
   L.wge_off = o;    o = round256(o + size_t(E) * 16);
   L.kbase_off = o;  o = round256(o + size_t(L.max_groups) * 4);
@@ -75,14 +75,16 @@ size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, 
 // weight-gradient row (kbase[group], a multiple of 32) in gradient-return
 // order, the owner group of every 32-row chunk, and the
 // experts present with their segment (first 32-row slice, slices), longest
-// segment first (ties: lower expert id), so the work counter of the
-// multi-problem launch hands out the longest tiles first. Zeroes that
-// counter.
+// segment first (ties: lower expert id), and how many of them have at least
+// long_slices slices (those tiles are handed out before the input-gradient
+// tiles, the shorter ones after them). Zeroes the work counter of the
+// multi-problem launch.
 __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
     int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase,
     int32_t *__restrict__ chunk_group, int4 *__restrict__ wg_experts, int32_t *__restrict__ n_wg,
-    int32_t *__restrict__ kslices, int32_t *__restrict__ queue) {
+    int32_t long_slices, int32_t *__restrict__ n_wg_long, int32_t *__restrict__ kslices,
+    int32_t *__restrict__ queue) {
   __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks], skb[kMaxChunks];
   __shared__ int32_t esl[LLEP_MAX_EXPERTS];
   const int tid = threadIdx.x;
@@ -122,10 +124,14 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     wg_experts[idx] = make_int4(e, start, sl, 0);
   }
   if (tid == 0) {
-    int32_t n = 0, tot = 0;
-    for (int e = 0; e < E; ++e) n += esl[e] > 0;
+    int32_t n = 0, nl = 0, tot = 0;
+    for (int e = 0; e < E; ++e) {
+      n += esl[e] > 0;
+      nl += esl[e] > 0 && esl[e] >= long_slices;
+    }
     for (int j = 0; j < G; ++j) tot += ssl[j];
     *n_wg = n;
+    *n_wg_long = nl;
     *kslices = tot;
     *queue = 0;
   }
@@ -354,6 +360,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   int32_t *n_wg = n_mtiles + 1;
   int32_t *kslices = n_mtiles + 2;
   int32_t *queue = n_mtiles + 3;
+  int32_t *n_wg_long = n_mtiles + 4;
   int4 *tiles = reinterpret_cast<int4 *>(ws + L.tiles_off);
   int4 *wge = reinterpret_cast<int4 *>(ws + L.wge_off);
   int32_t *kbase = reinterpret_cast<int32_t *>(ws + L.kbase_off);
@@ -375,7 +382,8 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   err = launch_tile_table(a.groups, a.group_begin, a.device, a.P, tiles, n_mtiles, stream);
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(wgrad_table_kernel, dim3(1), dim3(1024), 0, stream, a.groups, a.group_begin,
-                     a.device, a.P, a.E, a.E / a.P, kbase, chunk, wge, n_wg, kslices, queue);
+                     a.device, a.P, a.E, a.E / a.P, kbase, chunk, wge, n_wg, 2 * F / kSK,
+                     n_wg_long, kslices, queue);
   LLEP_CHECK_LAUNCH();
   constexpr int NT = 64 * kWavesM * kWavesN;
   constexpr int NT192 = 64 * kWavesM192 * kWavesN192;
@@ -455,6 +463,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   g3.wp[1] = WgProblem{actt, dot, wblk, a.dw_down, nullptr, int64_t(F) * D, F, D, 0};
   g3.wg_experts = wge;
   g3.n_wg = n_wg;
+  g3.n_wg_long = n_wg_long;
   g3.queue = queue;
   // 256 x 192 tiles: the 256 x 256 ring fills the LDS and leaves no room for
   // the work counter's broadcast slot
