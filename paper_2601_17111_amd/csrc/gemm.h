@@ -505,10 +505,14 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
   // The scheduling barriers keep that order, so the memory instructions issue
   // while the MFMAs execute instead of in bursts between them.
   constexpr int NM = TM * TN, NR = TM + TN, ND = A_PER_WAVE + B_SLOTS;
+  // DMA side operations of a slice in its first k-step (the rest in the
+  // second); every DMA-issuing wave issues at least D0 per slice
+  constexpr int D0 = PER_STAGE / 2;
+  static_assert(D0 <= PER_STAGE && (kAhead - 2) * PER_STAGE + D0 < 64, "wait count");
   // dma_wave: std::true_type for the waves that issue the DMA, else
   // std::false_type (their DMA side operations are empty)
-  auto side_op = [&](auto dma_wave, int q, int st_next, int ks_next, bf16x8 (&fa)[TM],
-                     bf16x8 (&fb)[TN], int st_dma, int kt_dma) {
+  auto side_op = [&](auto dma_wave, int q, int dma_lo, int st_next, int ks_next,
+                     bf16x8 (&fa)[TM], bf16x8 (&fb)[TN], int st_dma, int kt_dma) {
     constexpr bool kDmaWave = decltype(dma_wave)::value;
     if (q < TM) {
       const uint16_t *a_s = stageA(st_next);
@@ -519,7 +523,7 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
       fb[q - TM] = *reinterpret_cast<const bf16x8 *>(
           &b_s[lds_swz32(wn * WN + (q - TM) * 32 + (lane & 31), ks_next * 2 + (lane >> 5))]);
     } else if constexpr (kDmaWave) {
-      const int d = q - NR;
+      const int d = dma_lo + q - NR;
       const uint32_t a_st = sA0 + st_dma * STAGE_BYTES, b_st = sB0 + st_dma * STAGE_BYTES;
       const int kba = kABlocked ? kt_dma * 1024 : kt_dma * kSK * 2;
       const int kbb = kt_dma * 1024;
@@ -533,9 +537,9 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
   };
   auto interleaved_step = [&](auto dma_wave, f32x16 (&acc)[TM][TN], const bf16x8 (&fa)[TM],
                               const bf16x8 (&fb)[TN], bf16x8 (&fa_next)[TM],
-                              bf16x8 (&fb_next)[TN], int st_next, int ks_next, bool with_dma,
-                              int st_dma, int kt_dma) {
-    const int NS = NR + (with_dma ? ND : 0);
+                              bf16x8 (&fb_next)[TN], int st_next, int ks_next, int dma_lo,
+                              int dma_hi, int st_dma, int kt_dma) {
+    const int NS = NR + (dma_hi - dma_lo);
 #pragma unroll
     for (int s = 0; s < NM; ++s) {
       acc[s / TN][s % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -544,7 +548,7 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
 #pragma unroll
       for (int q = 0; q < NR + ND; ++q) {
         if (q < NS && q * NM >= s * NS && q * NM < (s + 1) * NS) {
-          side_op(dma_wave, q, st_next, ks_next, fa_next, fb_next, st_dma, kt_dma);
+          side_op(dma_wave, q, dma_lo, st_next, ks_next, fa_next, fb_next, st_dma, kt_dma);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -592,14 +596,19 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
       // others, so the DMA needs no per-instruction branch)
       auto steady = [&](auto dma_wave) {
         for (; kt < nk - kAhead; ++kt) {
-          // k-step 0 of slice kt; reads of its k-step 1; DMA of slice kt + kAhead
-          interleaved_step(dma_wave, acc, fa0, fb0, fa1, fb1, st, 1, true, st_req, kt_req);
+          // k-step 0 of slice kt; reads of its k-step 1; the first D0 DMA of
+          // slice kt + kAhead
+          interleaved_step(dma_wave, acc, fa0, fb0, fa1, fb1, st, 1, 0, D0, st_req, kt_req);
+          // slice kt + 1 has landed when at most the D0 of slice kt + kAhead
+          // and all of slices kt + 2 .. kt + kAhead - 1 are in flight
+          wait_and_sync<(kAhead - 2) * PER_STAGE + D0>();
+          st = next_stage(st);
+          // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1; the rest
+          // of the DMA of slice kt + kAhead (its stage, that of slice kt - 1,
+          // has been free since the previous barrier)
+          interleaved_step(dma_wave, acc, fa1, fb1, fa0, fb0, st, 0, D0, ND, st_req, kt_req);
           st_req = next_stage(st_req);
           ++kt_req;
-          wait_and_sync<(kAhead - 1) * PER_STAGE>();
-          st = next_stage(st);
-          // k-step 1 of slice kt; reads of k-step 0 of slice kt + 1
-          interleaved_step(dma_wave, acc, fa1, fb1, fa0, fb0, st, 0, false, 0, 0);
         }
       };
       if (wave < NWD)
