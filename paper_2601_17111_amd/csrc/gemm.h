@@ -132,9 +132,10 @@ typedef __attribute__((address_space(1))) void *gbl_void_ptr;
 
 constexpr int kSK = 32;      // k-slice per LDS stage
 constexpr int kAhead = 4;    // slices requested ahead of the one being read
-// One stage more than the look-ahead: slice kt+kAhead is requested before
-// the barrier that releases slice kt+1, into the buffer of slice kt-1 (free
-// since the previous barrier), so after a barrier the MFMAs restart at once.
+// One stage more than the look-ahead: slice kt+kAhead goes into the buffer
+// of slice kt-1 (free since the previous barrier), requested half before the
+// barrier that releases slice kt+1 and half after it, so after a barrier the
+// MFMAs restart at once.
 constexpr int kStages = kAhead + 1;
 
 // The DMA is issued through asm so the compiler does not treat it as a
@@ -588,8 +589,8 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
         wait_and_sync<0>();
       read_frags(st, 0, fa0, fb0);
       int kt = 0;
-      // steady state: request slice kt + kAhead, three slices stay in flight
-      // past slice kt + 1 (compile-time wait count). The last slice is peeled
+      // steady state: request slice kt + kAhead, two and a half slices stay
+      // in flight past slice kt + 1 (compile-time wait count). The last slice is peeled
       // so no branch joins around the LDS reads (the wait inserted at such a
       // join would drain the fresh reads).
       // (one copy of the loop for the DMA-issuing waves and one for the
