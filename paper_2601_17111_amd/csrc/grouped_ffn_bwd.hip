@@ -39,7 +39,8 @@ static BwdLayout bwd_layout(int64_t R, int32_t E, int32_t P, int32_t D, int32_t 
   L.max_mtiles = R / kTileM + L.max_groups + 1;
   L.prow_max = R + 16 * L.max_groups;
   L.kmax = (R + 32 * L.max_groups + 31) / 32 * 32;
-  size_t o = 256;  // counters: n_mtiles, n_wg, k-slices in use, work counter, long n_wg
+  size_t o = 256;  // counters: n_mtiles, n_wg, k-slices in use, work counter, long n_wg,
+                   // copy counter
   L.tiles_off = o;  o = round256(o + size_t(L.max_mtiles) * 16);
   L.wge_off = o;    o = round256(o + size_t(E) * 16);
   L.kbase_off = o;  o = round256(o + size_t(L.max_groups) * 4);
@@ -77,14 +78,14 @@ size_t ffn_backward_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t D, 
 // experts present with their segment (first 32-row slice, slices), longest
 // segment first (ties: lower expert id), and how many of them have at least
 // long_slices slices (those tiles are handed out before the input-gradient
-// tiles, the shorter ones after them). Zeroes the work counter of the
-// multi-problem launch.
+// tiles, the shorter ones after them). Zeroes the work counters of the
+// multi-problem launch and of the d act launch's copies.
 __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t device,
     int32_t P, int32_t E, int32_t M, int32_t *__restrict__ kbase,
     int32_t *__restrict__ chunk_group, int4 *__restrict__ wg_experts, int32_t *__restrict__ n_wg,
     int32_t long_slices, int32_t *__restrict__ n_wg_long, int32_t *__restrict__ kslices,
-    int32_t *__restrict__ queue) {
+    int32_t *__restrict__ queue, int32_t *__restrict__ copy_counter) {
   __shared__ int32_t se[kMaxChunks], skey[kMaxChunks], ssl[kMaxChunks], skb[kMaxChunks];
   __shared__ int32_t esl[LLEP_MAX_EXPERTS];
   const int tid = threadIdx.x;
@@ -134,46 +135,126 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     *n_wg_long = nl;
     *kslices = tot;
     *queue = 0;
+    *copy_counter = 0;
   }
 }
 
-// Copy C columns of the range's rows (row-major by x_perm row, ld elements)
-// into the weight-gradient layout: blocks of 16 columns x 32 rows over
-// [C][kmax], row kbase[g] + r of the layout = row r of group g (zero for the
-// padding r >= n_g).
-__global__ __launch_bounds__(256) void to_wgrad_kernel(
-    const uint16_t *__restrict__ src, int64_t ld, int32_t C, const int32_t *__restrict__ groups,
-    const int32_t *__restrict__ kbase, const int32_t *__restrict__ chunk_group,
-    const int32_t *__restrict__ kslices, int64_t kmax, uint16_t *__restrict__ dst) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][40];
-  const int t = threadIdx.x;
-  const int64_t items = int64_t(*kslices) * (C / 64);
-  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    const int c = int(item / (C / 64)), cc = int(item % (C / 64));
-    const int gi = chunk_group[c];
-    const int n = groups[4 * gi + 3];
-    const int r0 = c * 32 - kbase[gi];
-    {
-      const int r = t >> 3, col = cc * 64 + (t & 7) * 8;
-      i32x4 v = {0, 0, 0, 0};
-      const int row = r0 + r;
-      if (row < n)
-        v = *reinterpret_cast<const i32x4 *>(src + int64_t(groups[4 * gi + 2] + row) * ld + col);
+// The other weight-gradient operands: C columns of the range's rows
+// (row-major by x_perm row, ld elements) copied into the weight-gradient
+// layout, blocks of 16 columns x 32 rows over [C][kmax], row kbase[g] + r of
+// the layout = row r of group g (zero for the padding r >= n_g). Item i of a
+// source is its 32-row slice c = i / (C / 64) and its 64-column group
+// i % (C / 64); the two sources (X, d out) follow one another.
+struct WgradCopy {
+  const uint16_t *src[2];
+  uint16_t *dst[2];
+  int64_t ld;
+  int32_t C;  // a multiple of 64
+  int64_t kmax;
+  const int32_t *groups, *kbase, *chunk_group, *kslices;
+  int32_t *counter;  // items taken; zeroed by the table kernel
+};
+
+constexpr int kCopyBatch = 8;             // items per counter claim
+constexpr int kCopyTileBytes = 64 * 32 * 2;  // LDS staging tile of one wave
+
+// One wavefront copies items taken kCopyBatch at a time from w.counter until
+// none is left, with no barrier: each wave stages through its own LDS tile
+// (`tile`, kCopyTileBytes) of 64 columns x 32 rows, column-major, the four
+// 8-row chunks of column col in slots chunk ^ ((col / 8) % 4) so that a
+// write instruction spreads over the banks. The loads of a batch are all
+// issued before its first item is staged.
+__device__ __forceinline__ void wgrad_copy_items(const WgradCopy &w, uint16_t *tile) {
+  const int lane = threadIdx.x & 63;
+  const int cgroups = w.C / 64;
+  const int per_src = __builtin_amdgcn_readfirstlane(*w.kslices) * cgroups;
+  const int n_items = 2 * per_src;
+  // load layout: lane l holds row 8 q + l / 8 of the slice, columns
+  // 8 (l % 8) .. + 7 of the item's 64 (each load instruction covers 8 whole
+  // rows of 128 bytes)
+  const int a = lane & 7, b = lane >> 3;
+  const bool odd = b & 1;
+  for (;;) {
+    int b0 = 0;
+    if (lane == 0) b0 = atomicAdd(w.counter, kCopyBatch);
+    b0 = __builtin_amdgcn_readfirstlane(b0);
+    if (b0 >= n_items) break;
+    i32x4 v[kCopyBatch][4];
+#pragma unroll
+    for (int j = 0; j < kCopyBatch; ++j) {
+      const int i = min(b0 + j, n_items - 1);  // past the end: the last item again (not stored)
+      const int s = i >= per_src, rem = i - s * per_src;
+      const int c = rem / cgroups, cc = rem - c * cgroups;
+      const int gi = w.chunk_group[c];
+      const int n = w.groups[4 * gi + 3];
+      const int r0 = c * 32 - w.kbase[gi];
+      const uint16_t *src = w.src[s] + int64_t(w.groups[4 * gi + 2]) * w.ld + cc * 64 + a * 8;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        tile[(t & 7) * 8 + 2 * q][r] = uint16_t(uint32_t(v[q]) & 0xffffu);
-        tile[(t & 7) * 8 + 2 * q + 1][r] = uint16_t(uint32_t(v[q]) >> 16);
+        const int row = r0 + 8 * q + b;
+        v[j][q] = i32x4{0, 0, 0, 0};
+        if (row < n) v[j][q] = *reinterpret_cast<const i32x4 *>(src + int64_t(row) * w.ld);
       }
     }
-    __syncthreads();
-    {
-      const int b = t >> 6, o = t & 63;
-      const int lc = b * 16 + (o >> 2), k8 = (o & 3) * 8;
-      *reinterpret_cast<i32x4 *>(dst + (int64_t(cc * 4 + b) * (kmax / 32) + c) * 512 + (o >> 2) * 32 +
-                                 k8) = *reinterpret_cast<const i32x4 *>(&tile[lc][k8]);
+#pragma unroll
+    for (int j = 0; j < kCopyBatch; ++j) {
+      const int i = b0 + j;
+      if (i >= n_items) break;
+      const int s = i >= per_src, rem = i - s * per_src;
+      const int c = rem / cgroups, cc = rem - c * cgroups;
+      // the previous item's reads of the tile are done before it is rewritten
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // Lanes l and l ^ 8 hold rows r and r ^ 1 of the same columns: each
+      // writes one 32-bit word of two rows, the even-row lane for the even
+      // column of a pair, the odd-row lane for the odd one.
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t mine = uint32_t(v[j][q][e]);
+          const uint32_t other = uint32_t(__shfl_xor(int(mine), 8));
+          const uint32_t word = odd ? ((other >> 16) | (mine & 0xffff0000u))
+                                    : ((mine & 0xffffu) | (other << 16));
+          const int col = 8 * a + 2 * e + int(odd);
+          *reinterpret_cast<uint32_t *>(tile + col * 32 + ((q ^ (a & 3)) << 3) + (b & 6)) = word;
+        }
+      }
+      // the tile is written before any lane reads it back
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // block bb: columns 16 bb .. 16 bb + 15; lane l column l / 4, rows
+      // 8 (l % 4) .. + 7
+      uint16_t *dst = w.dst[s] + int64_t(c) * 512 + (lane >> 2) * 32 + (lane & 3) * 8;
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        const int col = bb * 16 + (lane >> 2);
+        *reinterpret_cast<i32x4 *>(dst + int64_t(cc * 4 + bb) * (w.kmax / 32) * 512) =
+            *reinterpret_cast<const i32x4 *>(tile + col * 32 + (((lane & 3) ^ ((col >> 3) & 3)) << 3));
+      }
     }
-    __syncthreads();
   }
+}
+
+// Step 2 of the backward (d act GEMM with the SwiGLU backward epilogue) and
+// the copies of X and d out into the weight-gradient layout in one launch:
+// the GEMM deals its tiles in rounds, so the workgroups without a tile in the
+// last, partly filled round start on the copies while the others finish
+// their tiles, and everyone takes copy items once its tiles are done.
+template <int BN, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
+__attribute__((amdgpu_waves_per_eu(WAVES_M * WAVES_N / 4, WAVES_M * WAVES_N / 4)))
+void dact_kernel(GemmArgs g, WgradCopy w) {
+  static_assert(WAVES_M * WAVES_N * kCopyTileBytes <= ring_bytes<BN>(), "copy tiles fit the ring");
+  __shared__ __attribute__((aligned(1024))) char smem[ring_bytes<BN>()];
+  __shared__ int32_t s_next;
+  {
+    LaunchSched<256, BN, false> sched(g, &s_next);
+    TileCoord t;
+    if (sched.first(t)) gemm_tiles<BN, WAVES_M, WAVES_N, kEpiSwigluBwd, false, true>(g, smem, t, sched);
+  }
+  // every wave is done with the ring (its last epilogue's staging reads)
+  // before the copies reuse it
+  __syncthreads();
+  wgrad_copy_items(w, reinterpret_cast<uint16_t *>(smem + (threadIdx.x >> 6) * kCopyTileBytes));
 }
 
 // Packed weights for the backward GEMMs, in the forward's block layout:
@@ -361,6 +442,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   int32_t *kslices = n_mtiles + 2;
   int32_t *queue = n_mtiles + 3;
   int32_t *n_wg_long = n_mtiles + 4;
+  int32_t *copy_counter = n_mtiles + 5;
   int4 *tiles = reinterpret_cast<int4 *>(ws + L.tiles_off);
   int4 *wge = reinterpret_cast<int4 *>(ws + L.wge_off);
   int32_t *kbase = reinterpret_cast<int32_t *>(ws + L.kbase_off);
@@ -383,7 +465,7 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(wgrad_table_kernel, dim3(1), dim3(1024), 0, stream, a.groups, a.group_begin,
                      a.device, a.P, a.E, a.E / a.P, kbase, chunk, wge, n_wg, 2 * F / kSK,
-                     n_wg_long, kslices, queue);
+                     n_wg_long, kslices, queue, copy_counter);
   LLEP_CHECK_LAUNCH();
   constexpr int NT = 64 * kWavesM * kWavesN;
   constexpr int NT192 = 64 * kWavesM192 * kWavesN192;
@@ -410,7 +492,9 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
     LLEP_CHECK_LAUNCH();
   }
   // 2. d act = d out Wd^T; the epilogue writes [d g | d u] blocked (for dX)
-  // and [d g | d u], act transposed into the weight-gradient layout
+  // and [d g | d u], act transposed into the weight-gradient layout; in the
+  // same launch, the other weight-gradient operands X and d out, with the
+  // rows of each expert laid end to end along k (gradient-return order)
   GemmArgs g2 = g;
   g2.A = static_cast<const uint16_t *>(a.d_out_perm);
   g2.lda = D;
@@ -426,25 +510,27 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
   g2.act_t = actt;
   g2.kbase = kbase;
   g2.kmax = L.kmax;
+  WgradCopy wc = {};
+  wc.src[0] = static_cast<const uint16_t *>(a.x_perm);
+  wc.src[1] = static_cast<const uint16_t *>(a.d_out_perm);
+  wc.dst[0] = xt;
+  wc.dst[1] = dot;
+  wc.ld = D;
+  wc.C = D;
+  wc.kmax = L.kmax;
+  wc.groups = a.groups;
+  wc.kbase = kbase;
+  wc.chunk_group = chunk;
+  wc.kslices = kslices;
+  wc.counter = copy_counter;
   if (f192)
-    hipLaunchKernelGGL((gemm256_kernel<192, kWavesM192, kWavesN192, kEpiSwigluBwd, false, true>),
-                       dim3(grid), dim3(NT192), 0, stream, g2);
+    hipLaunchKernelGGL((dact_kernel<192, kWavesM192, kWavesN192>), dim3(grid), dim3(NT192), 0,
+                       stream, g2, wc);
   else
-    hipLaunchKernelGGL((gemm256_kernel<256, kWavesM, kWavesN, kEpiSwigluBwd, false, true>),
-                       dim3(grid), dim3(NT), 0, stream, g2);
+    hipLaunchKernelGGL((dact_kernel<256, kWavesM, kWavesN>), dim3(grid), dim3(NT), 0, stream, g2,
+                       wc);
   LLEP_CHECK_LAUNCH();
-  // 3. the other weight-gradient operands, X and d out, with the rows of
-  // each expert laid end to end along k (gradient-return order)
-  const int tg = 4 * grid;
-  hipLaunchKernelGGL(to_wgrad_kernel, dim3(tg), dim3(256), 0, stream,
-                     static_cast<const uint16_t *>(a.x_perm), int64_t(D), D, a.groups, kbase,
-                     chunk, kslices, L.kmax, xt);
-  LLEP_CHECK_LAUNCH();
-  hipLaunchKernelGGL(to_wgrad_kernel, dim3(tg), dim3(256), 0, stream,
-                     static_cast<const uint16_t *>(a.d_out_perm), int64_t(D), D, a.groups, kbase,
-                     chunk, kslices, L.kmax, dot);
-  LLEP_CHECK_LAUNCH();
-  // 4. one launch: dX = [d g | d u] [Wg | Wu]^T into the x_perm rows, and
+  // 3. one launch: dX = [d g | d u] [Wg | Wu]^T into the x_perm rows, and
   // the weight gradients X^T [d g | d u] (de-interleaved into dWg, dWu) and
   // act^T d out, per expert over its k-segment
   GemmArgs g3 = g;
