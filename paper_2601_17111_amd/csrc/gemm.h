@@ -935,7 +935,8 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
         // 8k + l / 8 and columns 4 (l % 8) .. 4 (l % 8) + 3. (Stored straight
         // from the accumulators, every store instruction wrote 32-byte pieces
         // of 32 rows, and the many short tiles of the small experts were
-        // bound by those partial-line writes.)
+        // bound by those partial-line writes.) The stores are non-temporal:
+        // nothing in the call reads the gradients back.
         constexpr int RSF = 32 * 4 + 16;
         static_assert(32 * RSF <= STAGING, "staging");
         const int ld = gate_up ? (c.N >> 1) : c.N;  // fp32 elements per gradient row
@@ -965,7 +966,8 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
               const int r = 8 * k + rr;
               const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + r * RSF + rc * 4);
               if (i * 32 + r < rows_w)
-                *reinterpret_cast<f32x4 *>(base + int64_t(m0 + r) * ld + rc) = v;
+                __builtin_nontemporal_store(
+                    v, reinterpret_cast<f32x4 *>(base + int64_t(m0 + r) * ld + rc));
             }
           }
         }
