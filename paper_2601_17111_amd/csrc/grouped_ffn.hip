@@ -227,7 +227,9 @@ struct FusedSched {
   int nn, N, nk, total;  // n-tiles, columns, k-slices and tiles of the phase
   int cur;        // claiming wave: queues of this phase found empty so far
   int claimed;    // claiming wave: the tile claimed for after the running one
-  int32_t *mailbox;  // LDS word that broadcasts wave 0's claim
+  int4 pre_te;    // claiming wave: the claimed tile's list entry
+  int pre_e, pre_row0, pre_n;  // claiming wave: its group's expert, first row, rows
+  int32_t *mailbox;  // LDS words that broadcast the claiming wave's claim
 
   __device__ __forceinline__ FusedSched(const GemmArgs &g, const FusedFfnArgs f_, char *smem)
       : f(f_) {
@@ -265,9 +267,9 @@ struct FusedSched {
     }
     return -1;
   }
-  // all threads: the claiming wave's value (the mailbox is the first word of
-  // the ring: no slice may be in flight into it, and everyone has read it
-  // before the next barrier)
+  // all threads: the claiming wave's value (the mailbox is the first words
+  // of the ring: no slice may be in flight into them, and everyone has read
+  // them before the next barrier)
   __device__ __forceinline__ int broadcast(int v) {
     if (threadIdx.x == 64 * kClaimWave) *mailbox = v;
     __syncthreads();
@@ -304,12 +306,18 @@ struct FusedSched {
     locate(it, nt, mt);
     const int4 te = tiles[mt];
     const int32_t *gr = groups + 4 * te.x;
+    fill(it, te, gr[1], gr[2], gr[3], c);
+  }
+  __device__ __forceinline__ void fill(int it, int4 te, int e, int row0, int n,
+                                       TileCoord &c) const {
+    int nt, mt;
+    locate(it, nt, mt);
     c.grp = te.x;
-    c.e = gr[1];
-    c.row0 = gr[2];
+    c.e = e;
+    c.row0 = row0;
     c.prow0 = te.z;
     c.m0 = te.y * kTileM;
-    c.rows_valid = min(kTileM, gr[3] - c.m0);
+    c.rows_valid = min(kTileM, n - c.m0);
     c.N = N;
     c.n0 = nt * BN;
     c.cols_valid = min(BN, N - c.n0);
@@ -342,13 +350,24 @@ struct FusedSched {
   // that requests no slices (the first wave past the DMA-issuing half): it
   // waits only for the atomic, while every wave waits for the tile's first
   // slice, and keeps the answer in a scalar register until the main loop
-  // ends. Phase 1: the same wave also reads the claimed tile's count of
-  // finished gate/up tiles; when it is complete already, the tile need not
-  // poll it after the main loop.
+  // ends. It also reads the claimed tile's list entry and its group's
+  // expert, first row and row count, which next() hands to every wave
+  // through LDS: no global load then sits between this tile's main loop and
+  // the next tile's first requests (about 1% on the gpt-oss-120b shapes).
+  // Phase 1: the same wave also reads the claimed tile's count of finished
+  // gate/up tiles; when it is complete already, the tile need not poll it
+  // after the main loop.
   __device__ __forceinline__ void request() {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (wave == kClaimWave) {
       claimed = claim();
+      if (claimed >= 0) {
+        pre_te = tiles[mt_of(claimed)];
+        const int32_t *gr = groups + 4 * pre_te.x;
+        pre_e = gr[1];
+        pre_row0 = gr[2];
+        pre_n = gr[3];
+      }
       if (kPhase == 1 && claimed >= 0) {
         int v = 0;
         if (threadIdx.x == 64 * kClaimWave)
@@ -359,11 +378,24 @@ struct FusedSched {
     }
   }
   __device__ __forceinline__ bool next(TileCoord &t) {
+    if (threadIdx.x == 64 * kClaimWave) {
+      mailbox[1] = pre_te.x;
+      mailbox[2] = pre_te.y;
+      mailbox[3] = pre_te.z;
+      mailbox[4] = pre_e;
+      mailbox[5] = pre_row0;
+      mailbox[6] = pre_n;
+    }
     const int mine = claimed;
     const int v = broadcast(mine);
     const int it = v < 0 ? -1 : (v & ~kReadyFlag);
     if (it >= 0) {
-      decode(it, t);
+      const int4 te = {__builtin_amdgcn_readfirstlane(mailbox[1]),
+                       __builtin_amdgcn_readfirstlane(mailbox[2]),
+                       __builtin_amdgcn_readfirstlane(mailbox[3]), 0};
+      fill(it, te, __builtin_amdgcn_readfirstlane(mailbox[4]),
+           __builtin_amdgcn_readfirstlane(mailbox[5]), __builtin_amdgcn_readfirstlane(mailbox[6]),
+           t);
       if (kPhase == 1) wait_ready(t.mt, (v & kReadyFlag) != 0);
     }
     __syncthreads();  // mailbox read (and the wait done) before the ring fills
