@@ -14,8 +14,9 @@
 //                on atomics. The chunk table is copied to LDS first, so
 //                finding a pair's chunk reads no memory. Writes pair_row,
 //                row_pair and gate_perm.
-// gather_kernel  one wavefront per token: reads x[t] once (16-byte vectors)
-//                and writes it to the K rows of the token's pairs.
+// gather_kernel  one wavefront per 1 KB piece of a token's row (64 16-byte
+//                vectors): reads it once and writes it to the K rows of the
+//                token's pairs.
 #include "common.h"
 #include "kernels.h"
 
@@ -122,15 +123,18 @@ __global__ __launch_bounds__(256) void rank_kernel(
 // before storing the current one measured no faster, and one wave per
 // destination row (sequential writes, each token read K times) was 15-40%
 // slower (the gather moves its bytes at 5.9 TB/s, four fifths of them
-// writes; a plain fill reaches 6.8). Four pairs' rows of at most 4 vectors
-// per lane are in flight per combine step (1 or 2 measured within 2%).
+// writes; a plain fill reaches 6.8). One vector per lane (a wave per 1 KB
+// piece of a row, so each wave issues K stores) beats a wave per whole row
+// (6 vectors per lane, 6 K stores): 2-6% on the gpt-oss shapes, 5% on
+// deepseek-v3, 0.5% on qwen3; 2 or 3 vectors per lane fall in between.
+// Four pairs' rows of at most 4 vectors per lane are in flight per combine
+// step (1 or 2 measured within 2%).
 constexpr bool kGatherNtLoad = false;
 constexpr bool kGatherNtStore = false;
 constexpr bool kCombineNtLoad = true;
 constexpr bool kCombineNtStore = false;
 constexpr int kCombinePairs = 4;
 constexpr int kCombineMaxVecs = 4;
-constexpr int kGatherMaxVecs = 8;
 // Combine backward: non-temporal loads of out_perm and up to 6 vectors per
 // lane (one pass over a 2880-wide bf16 row) measured 359 -> 313 us on the
 // gpt-oss-120b layer (0.59 -> 0.68 of HBM peak).
@@ -159,9 +163,9 @@ inline int vecs_per_lane(int32_t vecs, int max_per_lane) {
   return (vpl + passes - 1) / passes;
 }
 
-// One wavefront per (token, slice of kV * 64 vectors of its row): the slice
-// is loaded once (all kV vectors per lane in flight) and stored to the rows
-// of the token's K pairs. Row indices come in as one vector load per 64 pairs and are read
+// One wavefront per (token, slice of kV * 64 vectors of its row; launched
+// with kV = 1): the slice is loaded once (all kV vectors per lane in flight)
+// and stored to the rows of the token's K pairs. Row indices come in as one vector load per 64 pairs and are read
 // back with v_readlane, so the stores need no further memory round trip.
 template <int kV>
 __global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x,
@@ -220,19 +224,9 @@ hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int32_t vecs = int32_t((int64_t(a.D) * a.elem_bytes) / 16);
-  const int kv = vecs_per_lane(vecs, kGatherMaxVecs);
-  const int64_t blocks = (a.T * ((vecs + kv * kWave - 1) / (kv * kWave)) + 3) / 4;
+  const int64_t blocks = (a.T * ((vecs + kWave - 1) / kWave) + 3) / 4;
   const int grid = int(blocks < 65536 ? blocks : 65536);
-  switch (kv) {
-    case 1: launch_gather_v<1>(grid, stream, a, vecs); break;
-    case 2: launch_gather_v<2>(grid, stream, a, vecs); break;
-    case 3: launch_gather_v<3>(grid, stream, a, vecs); break;
-    case 4: launch_gather_v<4>(grid, stream, a, vecs); break;
-    case 5: launch_gather_v<5>(grid, stream, a, vecs); break;
-    case 6: launch_gather_v<6>(grid, stream, a, vecs); break;
-    case 7: launch_gather_v<7>(grid, stream, a, vecs); break;
-    default: launch_gather_v<8>(grid, stream, a, vecs); break;
-  }
+  launch_gather_v<1>(grid, stream, a, vecs);
   return hipGetLastError();
 }
 
