@@ -128,7 +128,9 @@ __global__ __launch_bounds__(256) void rank_kernel(
 // (6 vectors per lane, 6 K stores): 2-6% on the gpt-oss shapes, 5% on
 // deepseek-v3, 0.5% on qwen3; 2 or 3 vectors per lane fall in between.
 // Four pairs' rows of at most 4 vectors per lane are in flight per combine
-// step (1 or 2 measured within 2%).
+// step (1 or 2 pairs measured within 2%; 1 or 2 vectors per lane, a wave
+// per 1 or 2 KB of the output row, within 1%: the combine's stream is
+// mostly reads).
 constexpr bool kGatherNtLoad = false;
 constexpr bool kGatherNtStore = false;
 constexpr bool kCombineNtLoad = true;
