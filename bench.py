@@ -255,6 +255,12 @@ def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps, flush):
     R = T * K
     t_ffn = seg["grouped_ffn_backward"] * 1e-3
     cb_bytes = T * D * 2 + 2 * R * D * 2 + 12 * R
+    # every expert with rows on d* gets its full float32 weight gradients
+    # (3 D F values), however few its rows: bytes the flop count leaves out
+    gb = L.bufs.group_begin.cpu().tolist()
+    experts = {int(e) for e in L.bufs.groups[gb[dstar]:gb[dstar + 1], 1].cpu().tolist()}
+    wgrad_bytes = len(experts) * 3 * D * F * 4
+    floor_s = 12.0 * D * F * n_rows / (PEAK_BF16_TFLOPS * 1e12) + wgrad_bytes / (PEAK_HBM_GBPS * 1e9)
     del gut, dnt
     L.gate_up = None
     return {
@@ -263,6 +269,12 @@ def _backward(layer, run, wg, wu, wd, cfg, dstar, n_rows, steps, flush):
         # forward); recomputing gate / up adds 4 D F
         "grouped_ffn_backward_TFLOPs": 12.0 * D * F * n_rows / t_ffn / 1e12,
         "grouped_ffn_backward_frac": 12.0 * D * F * n_rows / t_ffn / 1e12 / PEAK_BF16_TFLOPS,
+        # the MFMA work at the bf16 peak plus the float32 weight-gradient
+        # writes at the HBM peak, one after the other, over the measured time
+        "grouped_ffn_backward_experts": len(experts),
+        "grouped_ffn_backward_weight_gradient_GB": wgrad_bytes / 1e9,
+        "grouped_ffn_backward_floor_ms": floor_s * 1e3,
+        "grouped_ffn_backward_floor_frac": floor_s / t_ffn,
         "grouped_ffn_backward_recompute_ms": recompute_ms,
         "grouped_ffn_backward_recompute_TFLOPs":
             16.0 * D * F * n_rows / (recompute_ms * 1e-3) / 1e12,
