@@ -167,8 +167,8 @@ __global__ __launch_bounds__(256) void ffn_f32_down_kernel(
 // and n2 down-projection tiles (phase 1, BN2 columns of Wd each), each phase
 // in super-rows of kGroupM m-tiles (phase 0 m-tile fastest, as in the
 // two-launch form; phase 1 n-tile fastest). Every round of G tiles (G
-// workgroups) is dealt
-// in blocks of G / 8 consecutive tiles, one block per XCD, so that the
+// workgroups) is dealt in blocks of G / 8 consecutive tiles, one block per
+// XCD, so that the
 // tiles that run together on an XCD share operand panels in its L2 and the
 // XCDs work on neighbouring tiles; here each XCD takes the tiles of its
 // blocks from a counter, one at a time, and once its own are taken, those
