@@ -295,8 +295,9 @@ struct FusedSched {
     const int rem = u - sr * (kGroupM * nn);
     const int gm = min(kGroupM, n_mt - sr * kGroupM);
     if (kPhase == 1) {
-      // down-projection tiles by m-tile first: consecutive claims share an
-      // activation panel (fewer L2 misses: -7% fetched bytes, same time)
+      // down-projection tiles n-tile fastest: consecutive claims share an
+      // m-tile's activation panel (fewer L2 misses: -7% fetched bytes, same
+      // time)
       nt = rem % nn;
       mt = sr * kGroupM + rem / nn;
     } else {
