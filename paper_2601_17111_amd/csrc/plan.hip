@@ -11,10 +11,13 @@
 //
 // The assignment is sequential and greedy; it runs in one wavefront whose
 // lanes are the devices: lane d holds the assigned and pending loads g_a[d],
-// g_p[d] of Alg. 2. Sorting and table layout use the whole workgroup as
-// all-pairs counts over at most 2E + P chunks (a position is the number of
-// entries ahead of it), which needs two barriers instead of the dozens of a
-// sorting network or a tree scan.
+// g_p[d] of Alg. 2. The expert sort is an all-pairs count (a position is the
+// number of experts ahead of it) spread over the whole workgroup. The table
+// layout uses the order in which the greedy loop emits chunks: one expert's
+// chunks are consecutive and in start order, so a chunk's canonical index is
+// its expert's first canonical index plus its place in that run, and a
+// chunk's row needs only a count over the chunks of its own device (bucketed
+// by device) plus its expert's earlier chunks on the same device.
 #include "common.h"
 #include "kernels.h"
 
@@ -79,38 +82,39 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t *__restrict__ i
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / kWave;
 
-typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+// Tile counts of one expert column that a thread keeps in registers
+// between the two passes of the scan (and loads at once in either pass).
+constexpr int kScanHold = 32;
+static_assert(LLEP_MAX_EXPERTS <= kPlanThreads / 2 && LLEP_MAX_DEVICES <= kWave,
+              "two threads per expert in the scan, one lane per device");
 
-// Row-order key of a chunk: device, then expert, then emission index (the
-// emission order of one expert's chunks is their start order). The low 20
-// bits alone order chunks by (expert, start): the canonical order.
-constexpr uint32_t kKeyBits = 0x3ffffffu;
-constexpr uint32_t kRemoteFlag = 1u << 29;  // destination != native device
-constexpr uint32_t kHeadFlag = 1u << 30;    // first chunk of its (device, expert)
-static_assert(kMaxChunks <= 2048 && LLEP_MAX_EXPERTS <= 512 && LLEP_MAX_DEVICES <= 64,
-              "row keys pack 6 + 9 + 11 bits");
-
-__device__ __forceinline__ uint32_t row_key(int d, int e, int i) {
-  return (uint32_t(d) << 20) | (uint32_t(e) << 11) | uint32_t(i);
+// Sort key of expert e: larger load first, then smaller id (Alg. 2's order
+// with ties broken by id). Loads are non-negative.
+__device__ __forceinline__ uint64_t sort_key(int32_t load, int e) {
+  return (uint64_t(uint32_t(load)) << 32) | uint64_t(~uint32_t(e));
 }
 
 struct PlanShared {
-  // loads l[e], padded with -1 so 16-byte reads may run past E
-  __attribute__((aligned(16))) int32_t loads[LLEP_MAX_EXPERTS + 4];
+  int32_t loads[LLEP_MAX_EXPERTS];   // l[e]
   int32_t sorted[LLEP_MAX_EXPERTS];  // experts by load descending, id ascending
   i32x4 chunk[kMaxChunks];           // (device, expert, start, end), emission order
-  i32x2 key[kMaxChunks];             // (row key | remote flag, size)
-  i32x2 key5[kMaxChunks];            // the same with the head flag
-  int32_t row[kMaxChunks];           // first row of each chunk
+  int32_t slot[kMaxChunks];          // place of the chunk in its device's bucket
+  int32_t row_in[kMaxChunks];        // rows of earlier chunks of its (device, expert)
+  int32_t head[kMaxChunks];          // first chunk of its (device, expert)
+  int32_t bucket[kMaxChunks];        // chunks grouped by device
   int32_t part[kPlanThreads];        // tile-scan segment sums
-  int32_t e_cnt[LLEP_MAX_EXPERTS + 1];   // chunks per expert
-  int32_t d_groups[LLEP_MAX_DEVICES + 1];  // groups per device
-  int32_t dev_rows[LLEP_MAX_DEVICES];
-  int32_t n_chunks, forced, status, bypass, n_groups, n_xfers, total_rows;
+  int32_t e_first[LLEP_MAX_EXPERTS];       // emission index of each expert's first chunk
+  int32_t e_cnt[LLEP_MAX_EXPERTS + 1];     // chunks per expert -> canonical bases
+  int32_t e_xfers[LLEP_MAX_EXPERTS + 1];   // remote groups per expert -> transfer bases
+  int32_t d_chunks[LLEP_MAX_DEVICES + 1];  // chunks per device -> bucket bases
+  int32_t d_groups[LLEP_MAX_DEVICES + 1];  // groups per device -> group bases
+  int32_t dev_rows[LLEP_MAX_DEVICES + 1];  // rows per device
+  int32_t d_row0[LLEP_MAX_DEVICES + 1];    // first row of each device, then the total
+  int32_t n_chunks, forced, status, bypass, n_groups, n_xfers;
 };
 
-// Threads that share one chunk in the all-pairs passes over the chunk table
-// (a power of two dividing the wave, so a chunk's threads are adjacent lanes).
+// Threads that share one chunk in the pass over its device's bucket (a power
+// of two dividing the wave, so a chunk's threads are adjacent lanes).
 __device__ __forceinline__ int lanes_per_chunk(int nc) {
   return nc <= 64 ? 16 : nc <= 128 ? 8 : nc <= 256 ? 4 : nc <= 512 ? 2 : 1;
 }
@@ -121,8 +125,10 @@ __device__ __forceinline__ V group_sum(V v, int S) {
   return v;
 }
 
-// One whole wave: out[k] = in[0] + ... + in[k-1] for k < n (global store).
-__device__ void wave_exclusive_scan(const int32_t *in, int n, int32_t *out) {
+// One whole wave: out[k] = in[0] + ... + in[k-1] for k < n; out2, when given,
+// gets a copy.
+__device__ void wave_exclusive_scan(const int32_t *in, int n, int32_t *out,
+                                    int32_t *out2 = nullptr) {
   const int lane = lane_id();
   const int per = (n + kWave - 1) / kWave;
   const int k0 = min(n, lane * per), k1 = min(n, k0 + per);
@@ -135,8 +141,10 @@ __device__ void wave_exclusive_scan(const int32_t *in, int n, int32_t *out) {
   }
   int32_t run = incl - sum;
   for (int k = k0; k < k1; ++k) {
+    const int32_t v = in[k];
     out[k] = run;
-    run += in[k];
+    if (out2 != nullptr) out2[k] = run;
+    run += v;
   }
 }
 
@@ -149,45 +157,79 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   int32_t *rb = a.buf.rank_base;
 
   // ---- 1. scan tile counts: per-tile exclusive bases, and loads ----------
-  // Each expert's column of tile counts is split into G segments; loads go
-  // out eight at a time so a segment costs a few memory round trips.
+  // Each expert's column of tile counts is split into G segments. A segment
+  // of up to kScanHold tiles is loaded at once and kept in registers for the
+  // second pass, so the scan costs one memory round trip (plus the stores);
+  // longer segments take two passes of kScanHold loads at a time.
   {
     const int G = kPlanThreads / E;  // E <= 512: G >= 2
     const int e = tid % E, grp = tid / E;
     const int seg = (nt + G - 1) / G;
     const int t0 = grp * seg, t1 = grp < G ? min(nt, t0 + seg) : t0;
+    const bool hold = seg <= kScanHold;  // uniform
+    int bad = 0;
+    for (int t = tid; t < nt; t += kPlanThreads) bad |= rb[int64_t(nt) * E + t];
+    int32_t v[kScanHold];
     int32_t sum = 0;
-    for (int t = t0; t < t1; t += 8) {
-      int32_t v[8];
+    if (hold) {
+      // in steps of 8 up to the (uniform) segment length
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = t + u < t1 ? rb[int64_t(t + u) * E + e] : 0;
+      for (int u0 = 0; u0 < kScanHold; u0 += 8) {
+        if (u0 >= seg) break;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) sum += v[u];
+        for (int u = u0; u < u0 + 8; ++u) v[u] = t0 + u < t1 ? rb[int64_t(t0 + u) * E + e] : 0;
+      }
+#pragma unroll
+      for (int u0 = 0; u0 < kScanHold; u0 += 8) {
+        if (u0 >= seg) break;
+#pragma unroll
+        for (int u = u0; u < u0 + 8; ++u) sum += v[u];
+      }
+    } else {
+      for (int t = t0; t < t1; t += kScanHold) {
+#pragma unroll
+        for (int u = 0; u < kScanHold; ++u) v[u] = t + u < t1 ? rb[int64_t(t + u) * E + e] : 0;
+#pragma unroll
+        for (int u = 0; u < kScanHold; ++u) sum += v[u];
+      }
     }
     s.part[tid] = sum;
-    if (tid <= E) s.e_cnt[tid] = 0;
-    if (tid <= P) s.d_groups[tid] = 0;
-    if (tid < P) s.dev_rows[tid] = 0;
-    if (tid < 4) s.loads[E + tid] = -1;
-    __syncthreads();
+    if (tid <= E) {
+      s.e_cnt[tid] = 0;
+      s.e_xfers[tid] = 0;
+    }
+    if (tid <= P) {
+      s.d_chunks[tid] = 0;
+      s.d_groups[tid] = 0;
+      s.dev_rows[tid] = 0;
+    }
+    bad = __syncthreads_or(bad);
     if (grp < G) {
       int32_t run = 0;
       for (int g = 0; g < grp; ++g) run += s.part[g * E + e];
-      for (int t = t0; t < t1; t += 8) {
-        int32_t v[8];
+      if (hold) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = t + u < t1 ? rb[int64_t(t + u) * E + e] : 0;
+        for (int u0 = 0; u0 < kScanHold; u0 += 8) {
+          if (u0 >= seg) break;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          if (t + u < t1) rb[int64_t(t + u) * E + e] = run;
-          run += v[u];
+          for (int u = u0; u < u0 + 8; ++u) {
+            if (t0 + u < t1) rb[int64_t(t0 + u) * E + e] = run;
+            run += v[u];
+          }
+        }
+      } else {
+        for (int t = t0; t < t1; t += kScanHold) {
+#pragma unroll
+          for (int u = 0; u < kScanHold; ++u) v[u] = t + u < t1 ? rb[int64_t(t + u) * E + e] : 0;
+#pragma unroll
+          for (int u = 0; u < kScanHold; ++u) {
+            if (t + u < t1) rb[int64_t(t + u) * E + e] = run;
+            run += v[u];
+          }
         }
       }
       if (grp == G - 1) s.loads[e] = run;
     }
-    int bad = 0;
-    for (int t = tid; t < nt; t += kPlanThreads) bad |= rb[int64_t(nt) * E + t];
-    bad = __syncthreads_or(bad);
     if (tid == 0) {
       s.status = bad ? LLEP_STATUS_BAD_EXPERT_ID : 0;
       s.n_chunks = 0;
@@ -195,7 +237,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       s.bypass = 0;
       s.n_groups = 0;
       s.n_xfers = 0;
-      s.total_rows = 0;
     }
     __syncthreads();
   }
@@ -236,7 +277,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
         if (l > 0) {
           const int i = nc + __popcll(on & lanemask_lt());
           s.chunk[i] = i32x4{e / M, e, 0, l};
-          s.key[i] = i32x2{int32_t(row_key(e / M, e, i)), l};
         }
         nc += __popcll(on);
       }
@@ -244,21 +284,21 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     }
   } else {
     // Alg. 2: experts by load descending, id ascending. Position of expert e
-    // = number of experts ahead of it (all keys distinct).
-    if (tid < E) {
-      const int32_t le = s.loads[tid];
-      int32_t pos = 0;
-      const i32x4 *l4 = reinterpret_cast<const i32x4 *>(s.loads);
+    // = number of experts ahead of it (all keys distinct), counted by the G
+    // adjacent threads of e (a power of two, at most a wave), each taking
+    // every G-th expert.
+    {
+      int G = 1;
+      while (G < kWave && 2 * G * E <= kPlanThreads) G *= 2;
+      const int e = tid / G, q = tid % G;
+      if (e < E) {  // uniform over e's G lanes
+        const uint64_t ke = sort_key(s.loads[e], e);
+        int32_t pos = 0;
 #pragma unroll 8
-      for (int j4 = 0; j4 < (E + 3) / 4; ++j4) {
-        const i32x4 v = l4[j4];
-        const int j = 4 * j4;
-        pos += (v.x > le || (v.x == le && j < tid)) ? 1 : 0;
-        pos += (v.y > le || (v.y == le && j + 1 < tid)) ? 1 : 0;
-        pos += (v.z > le || (v.z == le && j + 2 < tid)) ? 1 : 0;
-        pos += (v.w > le || (v.w == le && j + 3 < tid)) ? 1 : 0;
+        for (int j = q; j < E; j += G) pos += sort_key(s.loads[j], j) > ke ? 1 : 0;
+        pos = group_sum(pos, G);
+        if (q == 0) s.sorted[pos] = e;
       }
-      s.sorted[pos] = tid;
     }
     __syncthreads();
 
@@ -280,11 +320,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       int nc = 0, forced = 0, overflow = 0;
       auto emit = [&](int d, int e, int ng, int64_t st, int64_t en) {
         if (nc < cmax) {
-          if (lane == 0) {
-            s.chunk[nc] = i32x4{d, e, int32_t(st), int32_t(en)};
-            s.key[nc] = i32x2{int32_t(row_key(d, e, nc) | (d != ng ? kRemoteFlag : 0u)),
-                              int32_t(en - st)};
-          }
+          if (lane == 0) s.chunk[nc] = i32x4{d, e, int32_t(st), int32_t(en)};
           ++nc;
         } else {
           overflow = 1;
@@ -306,10 +342,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
           // Case 1 for every expert in `fit`, in order
           if ((fit >> lane) & 1) {
             const int idx = nc + __popcll(fit & lanemask_lt());
-            if (idx < cmax) {
-              s.chunk[idx] = i32x4{nv, ev, 0, lv};
-              s.key[idx] = i32x2{int32_t(row_key(nv, ev, idx)), lv};
-            }
+            if (idx < cmax) s.chunk[idx] = i32x4{nv, ev, 0, lv};
           }
           nc += __popcll(fit);
           if (nc > cmax) {
@@ -380,93 +413,113 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   const int nc = s.n_chunks;
   const int S = lanes_per_chunk(nc);
 
-  // ---- 4. rows and the canonical chunk table ------------------------------
-  // Chunk i's first row is the total size of the chunks before it in row
-  // order; its canonical index is its position in (expert, start) order. Each
-  // chunk's S threads split the count over j.
-  for (int u = tid; u < nc * S; u += kPlanThreads) {
-    const int i = u / S, q = u % S;
-    const i32x2 wi = s.key[i];
-    const uint32_t ki = uint32_t(wi.x) & kKeyBits;
-    int32_t row = 0, canon = 0, dup = 0;
-#pragma unroll 8
-    for (int j = q; j < nc; j += S) {
-      const i32x2 wj = s.key[j];
-      const uint32_t kj = uint32_t(wj.x) & kKeyBits;
-      const bool before = kj < ki;
-      row += before ? wj.y : 0;
-      dup += (before && (kj >> 11) == (ki >> 11)) ? 1 : 0;
-      canon += (kj & 0xfffffu) < (ki & 0xfffffu) ? 1 : 0;
-    }
-    row = group_sum(row, S);
-    canon = group_sum(canon, S);
-    dup = group_sum(dup, S);
-    if (q == 0) {
-      const i32x4 ci = s.chunk[i];
-      const bool head = dup == 0;
-      s.row[i] = row;
-      s.key5[i] = i32x2{int32_t(uint32_t(wi.x) | (head ? kHeadFlag : 0u)), wi.y};
-      int32_t *cc = a.buf.chunks + 4 * canon;
-      cc[0] = ci.x;
-      cc[1] = ci.y;
-      cc[2] = ci.z;
-      cc[3] = ci.w;
-      a.buf.chunk_row[canon] = row;
-      atomicAdd(&s.dev_rows[ci.x], wi.y);
-      atomicAdd(&s.total_rows, wi.y);
-      atomicAdd(&s.e_cnt[ci.y], 1);
-      if (head) {
-        atomicAdd(&s.d_groups[ci.x], 1);
-        atomicAdd(&s.n_groups, 1);
-        if (uint32_t(wi.x) & kRemoteFlag) atomicAdd(&s.n_xfers, 1);
-      }
-    }
+  // ---- 4. table layout ----------------------------------------------------
+  // Both assignments emit one expert's chunks consecutively and in start
+  // order. Row order is (device, expert, start); canonical order is (expert,
+  // start).
+  // (a) per chunk: its expert's first chunk, its place in its device's
+  //     bucket, and the per-expert chunk and per-device row counts.
+  for (int i = tid; i < nc; i += kPlanThreads) {
+    const i32x4 ci = s.chunk[i];
+    if (i == 0 || s.chunk[i - 1].y != ci.y) s.e_first[ci.y] = i;
+    s.slot[i] = atomicAdd(&s.d_chunks[ci.x], 1);
+    atomicAdd(&s.e_cnt[ci.y], 1);
+    atomicAdd(&s.dev_rows[ci.x], ci.w - ci.z);
   }
   __syncthreads();
-
-  // ---- 5. groups, transfers, per-device and per-expert offsets -----------
-  // Group of a head chunk = heads before it in row order; its size sums the
-  // chunks of its (device, expert). Transfer of a remote head = remote heads
-  // before it in (expert, device) order: unique (expert, destination) pairs
-  // whose destination is not the expert's native device.
-  for (int u = tid; u < nc * S; u += kPlanThreads) {
-    const int i = u / S, q = u % S;
-    const i32x2 wi = s.key5[i];
-    if (!(uint32_t(wi.x) & kHeadFlag)) continue;  // uniform over the chunk's S threads
-    const uint32_t ki = uint32_t(wi.x) & kKeyBits;
-    const uint32_t xi = (((ki >> 11) & 511u) << 6) | (ki >> 20);
-    int32_t g = 0, n = 0, x = 0;
-#pragma unroll 8
-    for (int j = q; j < nc; j += S) {
-      const i32x2 wj = s.key5[j];
-      const uint32_t kj = uint32_t(wj.x) & kKeyBits;
-      const uint32_t xj = (((kj >> 11) & 511u) << 6) | (kj >> 20);
-      n += (kj >> 11) == (ki >> 11) ? wj.y : 0;
-      g += ((uint32_t(wj.x) & kHeadFlag) && kj < ki) ? 1 : 0;
-      x += ((uint32_t(wj.x) & kHeadFlag) && (uint32_t(wj.x) & kRemoteFlag) && xj < xi) ? 1 : 0;
+  // (b) per chunk: rows of its expert's earlier chunks on the same device
+  //     (none: it heads a group); group and transfer counts. Scans of the
+  //     counts so far: canonical bases, bucket bases, device first rows.
+  for (int i = tid; i < nc; i += kPlanThreads) {
+    const i32x4 ci = s.chunk[i];
+    int32_t before = 0, head = 1;
+    for (int j = s.e_first[ci.y]; j < i; ++j) {
+      const i32x4 cj = s.chunk[j];
+      if (cj.x == ci.x) {
+        before += cj.w - cj.z;
+        head = 0;
+      }
     }
-    g = group_sum(g, S);
-    n = group_sum(n, S);
-    x = group_sum(x, S);
-    if (q == 0) {
-      const int dev = int(ki >> 20), exp = int((ki >> 11) & 511u);
-      int32_t *gr = a.buf.groups + 4 * g;
-      gr[0] = dev;
-      gr[1] = exp;
-      gr[2] = s.row[i];
-      gr[3] = n;
-      if (uint32_t(wi.x) & kRemoteFlag) {
-        int32_t *xr = a.buf.xfers + 3 * x;
-        xr[0] = exp;
-        xr[1] = exp / M;
-        xr[2] = dev;
+    s.row_in[i] = before;
+    s.head[i] = head;
+    if (head) {
+      atomicAdd(&s.d_groups[ci.x], 1);
+      atomicAdd(&s.n_groups, 1);
+      if (ci.x != ci.y / M) {
+        atomicAdd(&s.e_xfers[ci.y], 1);
+        atomicAdd(&s.n_xfers, 1);
       }
     }
   }
-  // expert_chunk_begin = exclusive scan of chunks per expert (last wave);
-  // group_begin = exclusive scan of groups per device (the wave before it)
-  if (wave == kPlanWaves - 1) wave_exclusive_scan(s.e_cnt, E + 1, a.buf.expert_chunk_begin);
-  if (wave == kPlanWaves - 2) wave_exclusive_scan(s.d_groups, P + 1, a.buf.group_begin);
+  if (wave == kPlanWaves - 1) wave_exclusive_scan(s.e_cnt, E + 1, s.e_cnt, a.buf.expert_chunk_begin);
+  if (wave == kPlanWaves - 2) wave_exclusive_scan(s.d_chunks, P + 1, s.d_chunks);
+  if (wave == kPlanWaves - 3) wave_exclusive_scan(s.dev_rows, P + 1, s.d_row0);
+  __syncthreads();
+  // (c) bucket the chunks by device; scans of the group and transfer counts.
+  for (int i = tid; i < nc; i += kPlanThreads) s.bucket[s.d_chunks[s.chunk[i].x] + s.slot[i]] = i;
+  if (wave == kPlanWaves - 1) wave_exclusive_scan(s.e_xfers, E + 1, s.e_xfers);
+  if (wave == kPlanWaves - 2) wave_exclusive_scan(s.d_groups, P + 1, s.d_groups, a.buf.group_begin);
+  __syncthreads();
+  // (d) per chunk, S threads over its device's bucket: rows and groups of
+  //     smaller experts on the device give its row and group index; its
+  //     expert's run of chunks gives its canonical index, its group's size and
+  //     its transfer index (remote groups of the expert on smaller devices).
+  //     Every index is checked against its table before the store.
+  for (int u = tid; u < nc * S; u += kPlanThreads) {
+    const int i = u / S, q = u % S;
+    const i32x4 ci = s.chunk[i];
+    const int b0 = s.d_chunks[ci.x], b1 = s.d_chunks[ci.x + 1];
+    int32_t rows = 0, heads = 0;
+#pragma unroll 4
+    for (int k = b0 + q; k < b1; k += S) {
+      const int j = s.bucket[k];
+      const i32x4 cj = s.chunk[j];
+      if (cj.y < ci.y) {
+        rows += cj.w - cj.z;
+        heads += s.head[j];
+      }
+    }
+    rows = group_sum(rows, S);
+    heads = group_sum(heads, S);
+    if (q == 0) {
+      const int32_t row = s.d_row0[ci.x] + rows + s.row_in[i];
+      const int f = s.e_first[ci.y];
+      const int canon = s.e_cnt[ci.y] + (i - f);
+      if (canon >= 0 && canon < nc) {
+        int32_t *cc = a.buf.chunks + 4 * canon;
+        cc[0] = ci.x;
+        cc[1] = ci.y;
+        cc[2] = ci.z;
+        cc[3] = ci.w;
+        a.buf.chunk_row[canon] = row;
+      }
+      if (s.head[i]) {
+        const bool remote = ci.x != ci.y / M;
+        const int f1 = min(nc, s.e_cnt[ci.y + 1] - s.e_cnt[ci.y] + f);
+        int32_t n = 0, x = 0;
+        for (int j = f; j < f1; ++j) {
+          const i32x4 cj = s.chunk[j];
+          if (cj.x == ci.x) n += cj.w - cj.z;
+          if (s.head[j] && cj.x < ci.x && cj.x != ci.y / M) ++x;
+        }
+        const int g = s.d_groups[ci.x] + heads;
+        if (g >= 0 && g < s.n_groups) {
+          int32_t *gr = a.buf.groups + 4 * g;
+          gr[0] = ci.x;
+          gr[1] = ci.y;
+          gr[2] = row;
+          gr[3] = n;
+        }
+        x += s.e_xfers[ci.y];
+        if (remote && x >= 0 && x < s.n_xfers) {
+          int32_t *xr = a.buf.xfers + 3 * x;
+          xr[0] = ci.y;
+          xr[1] = ci.y / M;
+          xr[2] = ci.x;
+        }
+      }
+    }
+  }
   if (tid < P) a.buf.device_rows[tid] = s.dev_rows[tid];
 
   // ---- 6. summary ----------------------------------------------------------
@@ -482,7 +535,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     info.bypassed = (a.mode == LLEP_MODE_LLEP && P > 1 && use_ep) ? 1 : 0;
     info.forced = s.forced;
     info.max_device = best;
-    info.total_rows = s.total_rows;
+    info.total_rows = s.d_row0[P];
     *a.buf.info = info;
   }
 }
