@@ -289,7 +289,8 @@ constexpr uint32_t ring_bytes() {
 //              barrier: true with t the next tile of this loop (its first
 //              slices are requested during the epilogue), false when this
 //              loop ends after the current tile;
-//   done(c)    all threads, after tile c's epilogue (its stores issued);
+//   done(c, more)  all threads, after tile c's epilogue (its stores issued;
+//              more: another tile of this loop follows);
 //   kCoherentC whether C is stored device-coherent (read by other tiles of
 //              the same launch).
 //
@@ -347,7 +348,7 @@ struct LaunchSched {
     // tile's coordinates stay in scalar registers)
     return decode(kMulti ? __builtin_amdgcn_readfirstlane(*s_next) : it * G + slot, t);
   }
-  __device__ __forceinline__ void done(const TileCoord &) {}
+  __device__ __forceinline__ void done(const TileCoord &, bool) {}
 };
 
 // A is row-major (lda) or, with kABlocked, in 16 x 32 blocks over padded
@@ -1012,7 +1013,7 @@ __device__ __forceinline__ void gemm_tiles(const GemmArgs g, char *smem, TileCoo
         rowmajor_epilogue();
       }
     }
-    sched.done(c);
+    sched.done(c, more);
     if (more) {
       // the staging area is the last stages of the ring again: every wave's
       // staging reads are done (lgkmcnt) before slice kAhead - 1 may land

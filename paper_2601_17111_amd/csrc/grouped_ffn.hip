@@ -230,6 +230,7 @@ struct FusedSched {
   int claimed;    // claiming wave: the tile claimed for after the running one
   int4 pre_te;    // claiming wave: the claimed tile's list entry
   int pre_e, pre_row0, pre_n;  // claiming wave: its group's expert, first row, rows
+  int pending;    // phase 0: m-tile of the previous tile, not yet counted (or -1)
   int32_t *mailbox;  // LDS words that broadcast the claiming wave's claim
 
   __device__ __forceinline__ FusedSched(const GemmArgs &g, const FusedFfnArgs f_, char *smem)
@@ -246,6 +247,7 @@ struct FusedSched {
     nk = g.Kdim / kSK;
     cur = 0;
     claimed = -1;
+    pending = -1;
     mailbox = reinterpret_cast<int32_t *>(smem);
   }
   // tiles of the phase in XCD y's blocks
@@ -387,6 +389,14 @@ struct FusedSched {
     }
   }
   __device__ __forceinline__ bool next(TileCoord &t) {
+    // the previous tile's activation stores completed in every wave before
+    // the barrier that closed this tile's main loop (its last wait is for
+    // all memory operations): count that tile now
+    if (kPhase == 0 && pending >= 0) {
+      if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(f.done + pending, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      pending = -1;
+    }
     if (threadIdx.x == 64 * kClaimWave) {
       mailbox[1] = pre_te.x;
       mailbox[2] = pre_te.y;
@@ -414,9 +424,17 @@ struct FusedSched {
   // They were stored device-coherent (written through the L2), so once every
   // wave's stores have completed they are in memory for readers on any XCD:
   // no L2 writeback is needed before the count is raised (a writeback of the
-  // whole L2, even one not waited for, cost 5-7% of the call).
-  __device__ __forceinline__ void done(const TileCoord &c) {
+  // whole L2, even one not waited for, cost 5-7% of the call). When another
+  // phase-0 tile follows, the count waits for the end of that tile's main
+  // loop (next()), so the stores drain behind its first slices instead of
+  // holding every wave here; the workgroup's last phase-0 tile is counted
+  // at once, before any phase-1 tile is claimed or waited for.
+  __device__ __forceinline__ void done(const TileCoord &c, bool more) {
     if (kPhase != 0) return;
+    if (more) {
+      pending = c.mt;
+      return;
+    }
     wait_and_sync<0>();  // every wave's stores have completed
     if (threadIdx.x == 0)
       __hip_atomic_fetch_add(f.done + c.mt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
