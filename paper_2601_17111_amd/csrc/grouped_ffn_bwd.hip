@@ -100,8 +100,11 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
     ssl[i] = (n + 31) / 32;
   }
   __syncthreads();
+  // (the loops over groups and experts below are unrolled so that their
+  // LDS reads, which do not depend on one another, are in flight together)
   for (int i = tid; i < G; i += blockDim.x) {
     int32_t kb = 0;
+#pragma unroll 8
     for (int j = 0; j < G; ++j)
       if (se[j] < se[i] || (se[j] == se[i] && skey[j] < skey[i])) kb += ssl[j];
     kbase[lo + i] = kb * 32;
@@ -109,33 +112,46 @@ __global__ __launch_bounds__(1024) void wgrad_table_kernel(
   }
   for (int e = tid; e < E; e += blockDim.x) {
     int32_t sl = 0;
+#pragma unroll 8
     for (int j = 0; j < G; ++j) sl += se[j] == e ? ssl[j] : 0;
     esl[e] = sl;
   }
   __syncthreads();
-  // owner group of every 32-row slice, all threads striding over each group
-  for (int i = 0; i < G; ++i)
-    for (int c = skb[i] + tid; c < skb[i] + ssl[i]; c += blockDim.x) chunk_group[c] = lo + i;
+  // owner group of every 32-row slice: one wave per group, its lanes
+  // striding over the group's slices
+  for (int i = tid / kWave; i < G; i += blockDim.x / kWave)
+    for (int c = skb[i] + tid % kWave; c < skb[i] + ssl[i]; c += kWave) chunk_group[c] = lo + i;
   for (int e = tid; e < E; e += blockDim.x) {
     const int32_t sl = esl[e];
     if (sl == 0) continue;
     int32_t idx = 0, start = 0;
+#pragma unroll 8
     for (int f = 0; f < E; ++f) idx += esl[f] > sl || (esl[f] == sl && f < e);
+#pragma unroll 8
     for (int j = 0; j < G; ++j) start += se[j] < e ? ssl[j] : 0;
     wg_experts[idx] = make_int4(e, start, sl, 0);
   }
-  if (tid == 0) {
+  // counts over the experts and groups: one wave, lanes striding, then a
+  // wave sum
+  if (tid < kWave) {
     int32_t n = 0, nl = 0, tot = 0;
-    for (int e = 0; e < E; ++e) {
+    for (int e = tid; e < E; e += kWave) {
       n += esl[e] > 0;
       nl += esl[e] > 0 && esl[e] >= long_slices;
     }
-    for (int j = 0; j < G; ++j) tot += ssl[j];
-    *n_wg = n;
-    *n_wg_long = nl;
-    *kslices = tot;
-    *queue = 0;
-    *copy_counter = 0;
+    for (int j = tid; j < G; j += kWave) tot += ssl[j];
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      n += __shfl_xor(n, off);
+      nl += __shfl_xor(nl, off);
+      tot += __shfl_xor(tot, off);
+    }
+    if (tid == 0) {
+      *n_wg = n;
+      *n_wg_long = nl;
+      *kslices = tot;
+      *queue = 0;
+      *copy_counter = 0;
+    }
   }
 }
 
