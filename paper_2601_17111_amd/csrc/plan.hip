@@ -18,6 +18,8 @@
 // its expert's first canonical index plus its place in that run, and a
 // chunk's row needs only a count over the chunks of its own device (bucketed
 // by device) plus its expert's earlier chunks on the same device.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -123,6 +125,25 @@ template <typename V>
 __device__ __forceinline__ V group_sum(V v, int S) {
   for (int off = 1; off < S; off <<= 1) v += __shfl_xor(v, off);
   return v;
+}
+
+// One whole wave: the minimum of x over its 64 lanes, in every lane. Row
+// shifts by 1, 2, 4 and 8 leave each 16-lane row's minimum in its last lane;
+// two row broadcasts carry those into lane 63. A lane whose DPP source lies
+// outside its row, or in a row the step does not write, keeps its own value.
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+  auto step = [&](auto ctrl, auto rows) {
+    const uint32_t y = uint32_t(__builtin_amdgcn_update_dpp(int(x), int(x), decltype(ctrl)::value,
+                                                            decltype(rows)::value, 0xf, false));
+    x = min(x, y);
+  };
+  step(std::integral_constant<int, 0x111>{}, std::integral_constant<int, 0xf>{});  // row_shr:1
+  step(std::integral_constant<int, 0x112>{}, std::integral_constant<int, 0xf>{});  // row_shr:2
+  step(std::integral_constant<int, 0x114>{}, std::integral_constant<int, 0xf>{});  // row_shr:4
+  step(std::integral_constant<int, 0x118>{}, std::integral_constant<int, 0xf>{});  // row_shr:8
+  step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xa>{});  // row_bcast:15
+  step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xc>{});  // row_bcast:31
+  return uint32_t(__builtin_amdgcn_readlane(int(x), 63));
 }
 
 // One whole wave: out[k] = in[0] + ... + in[k-1] for k < n; out2, when given,
@@ -370,18 +391,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
           // m and r) every later one is skipped too and the force-assign goes
           // back to that first device: each round is one argmin over the
           // other devices (lowest index among ties).
-          const uint64_t others = dev_mask & ~(uint64_t(1) << ng);
+          const bool other = ((dev_mask >> lane) & 1) && lane != ng;
           while (r > 0) {
-            int32_t best = 0;
-            int o = -1;
-            for (uint64_t mm = others; mm != 0; mm &= mm - 1) {
-              const int d = __builtin_ctzll(mm);
-              const int32_t v = __builtin_amdgcn_readlane(S, d);
-              if (o < 0 || v < best) {
-                best = v;
-                o = d;
-              }
-            }
+            // the smallest S among the other devices (S >= 0, so unsigned
+            // order is S's order), then the lowest lane that holds it
+            const uint32_t least = wave_min_u32(other ? uint32_t(S) : 0xffffffffu);
+            const int o = __builtin_ctzll(__ballot(other && uint32_t(S) == least));
+            const int32_t best = int32_t(least);
             const int64_t room = cap - int64_t(best);
             int64_t c;
             if (room >= r) {
