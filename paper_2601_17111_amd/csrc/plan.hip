@@ -41,22 +41,30 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t *__restrict__ i
                                                    int32_t *__restrict__ rank_base) {
   extern __shared__ int32_t cnt[];  // [kRankWaves][E]
   const int tid = threadIdx.x;
-  for (int i = tid; i < kRankWaves * E; i += blockDim.x) cnt[i] = 0;
-  __syncthreads();
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int nb = bits_for(uint32_t(E));
   const int64_t s0 = int64_t(blockIdx.x) * kRankTile + int64_t(w) * kRankSub;
   int32_t *wcnt = cnt + w * E;
   int bad = 0;
-  for (int j = 0; j < kRankSub; j += kWave) {
-    if (s0 + j >= R) break;  // uniform in the wave
-    const int64_t p = s0 + j + lane_id();
-    uint32_t e = uint32_t(E);  // sentinel: past the end or invalid
-    if (p < R) {
-      const int32_t v = ids[p];
-      if (v >= 0 && v < E) e = uint32_t(v);
-      else bad = 1;
-    }
+  // all of the slice's ids are requested, before the counts are cleared,
+  // and only then counted (a pair past the end reads the last pair's id, in
+  // bounds, and is dropped)
+  constexpr int kPer = kRankSub / kWave;
+  int32_t raw[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int64_t p = s0 + j * kWave + lane_id();
+    raw[j] = ids[p < R ? p : R - 1];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // the loads issue together
+  for (int i = tid; i < kRankWaves * E; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const bool in = s0 + j * kWave + lane_id() < R;
+    const bool ok = raw[j] >= 0 && raw[j] < E;
+    if (in && !ok) bad = 1;
+    const uint32_t e = in && ok ? uint32_t(raw[j]) : uint32_t(E);  // sentinel: past the end or invalid
     const uint64_t m = match_any(e, nb);
     // one leader lane per expert value: no two lanes add to the same count
     if (e < uint32_t(E) && (m & lanemask_lt()) == 0) wcnt[e] += __popcll(m);
