@@ -45,37 +45,73 @@ __global__ __launch_bounds__(256) void rank_kernel(
   const int sub = int(blockIdx.x % kRankWaves);
   const int64_t p = int64_t(blockIdx.x) * kRankSub + w * kWave + lane_id();
   static_assert(kRankSub == kRankWaves * kWave, "a slice is one 64-pair block per wave");
-  // Every global load is issued up front (the pair's id and gate, the
-  // slice's base ranks, the chunk table), so the kernel waits on memory once.
+  // Every global load is issued up front, before any is waited for: the
+  // pair's id and gate, the slice's base counts (all of the tile's earlier
+  // slices' counts, summed afterwards for the ones before this slice), the
+  // chunk count and the chunk table (read up to the table's capacity, so no
+  // load waits for the count). Indices past the valid range are clamped
+  // into it and their values dropped.
+  constexpr int kThreads = kRankWaves * kWave;
+  const int64_t pc = p < R ? p : R - 1;
+  const int32_t id_raw = ids[pc];
+  const float gate_raw = gates[pc];
+  constexpr int kBaseIter = (LLEP_MAX_EXPERTS + kThreads - 1) / kThreads;
+  const int32_t *slice_cnt = rank_base + int64_t(n_tiles) * (E + 1) + tile * kRankWaves * E;
+  int32_t tb[kBaseIter], sc[kBaseIter][kRankWaves - 1];
+#pragma unroll
+  for (int i = 0; i < kBaseIter; ++i) {
+    const int ec = min(tid + kThreads * i, E - 1);
+    tb[i] = rank_base[tile * E + ec];
+#pragma unroll
+    for (int v = 0; v < kRankWaves - 1; ++v) sc[i][v] = slice_cnt[v * E + ec];
+  }
+  const int ncap = min(max_chunks, kMaxChunks);
+  const int32_t nc_raw = expert_chunk_begin[E];
+  constexpr int kEcbIter = (LLEP_MAX_EXPERTS + 1 + kThreads - 1) / kThreads;
+  int32_t ecbv[kEcbIter];
+#pragma unroll
+  for (int j = 0; j < kEcbIter; ++j) ecbv[j] = expert_chunk_begin[min(tid + kThreads * j, E)];
+  constexpr int kChunkIter = (kMaxChunks + kThreads - 1) / kThreads;
+  int32_t cs[kChunkIter], ce[kChunkIter], cr[kChunkIter];
+#pragma unroll
+  for (int k = 0; k < kChunkIter; ++k) {
+    const int cc = min(tid + kThreads * k, ncap - 1);
+    cs[k] = chunks[4 * cc + 2];
+    ce[k] = chunks[4 * cc + 3];
+    cr[k] = chunk_row[cc];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // the loads above issue together
   uint32_t ev = uint32_t(E);  // sentinel: past the end or invalid
   float gv = 0.0f;
   if (p < R) {
-    const int32_t v = ids[p];
-    gv = gates[p];
-    if (v >= 0 && v < E) ev = uint32_t(v);
+    gv = gate_raw;
+    if (id_raw >= 0 && id_raw < E) ev = uint32_t(id_raw);
   }
   // base rank of each expert in this slice: the tile's base (the plan's
   // scan of the tile counts) plus the counts of the tile's earlier slices
-  constexpr int kBaseIter = (LLEP_MAX_EXPERTS + 255) / 256;
-  const int32_t *slice_cnt = rank_base + int64_t(n_tiles) * (E + 1) + tile * kRankWaves * E;
   int32_t sb[kBaseIter];
 #pragma unroll
   for (int i = 0; i < kBaseIter; ++i) {
-    const int e = tid + 256 * i;
-    int32_t b = 0;
-    if (e < E) {
-      b = rank_base[tile * E + e];
-      for (int v = 0; v < sub; ++v) b += slice_cnt[v * E + e];
-    }
-    sb[i] = b;
+    int32_t b = tb[i];
+#pragma unroll
+    for (int v = 0; v < kRankWaves - 1; ++v) b += v < sub ? sc[i][v] : 0;
+    sb[i] = tid + kThreads * i < E ? b : 0;
   }
-  const int nc = min(max(expert_chunk_begin[E], 0), min(max_chunks, kMaxChunks));
-  for (int i = tid; i < kRankWaves * E; i += blockDim.x) wbase[i] = 0;
-  for (int i = tid; i <= E; i += blockDim.x) ecb[i] = min(max(expert_chunk_begin[i], 0), nc);
-  for (int c = tid; c < nc; c += blockDim.x) {
-    c_start[c] = chunks[4 * c + 2];
-    c_end[c] = chunks[4 * c + 3];
-    c_row[c] = chunk_row[c];
+  const int nc = min(max(nc_raw, 0), ncap);
+  for (int i = tid; i < kRankWaves * E; i += kThreads) wbase[i] = 0;
+#pragma unroll
+  for (int j = 0; j < kEcbIter; ++j) {
+    const int i = tid + kThreads * j;
+    if (i <= E) ecb[i] = min(max(ecbv[j], 0), nc);
+  }
+#pragma unroll
+  for (int k = 0; k < kChunkIter; ++k) {
+    const int c = tid + kThreads * k;
+    if (c < nc) {
+      c_start[c] = cs[k];
+      c_end[c] = ce[k];
+      c_row[c] = cr[k];
+    }
   }
   __syncthreads();
   // per-wave counts of each expert (one leader lane per expert value)
@@ -85,7 +121,7 @@ __global__ __launch_bounds__(256) void rank_kernel(
   // wave bases = slice base + counts of the slice's earlier waves
 #pragma unroll
   for (int i = 0; i < kBaseIter; ++i) {
-    const int e = tid + 256 * i;
+    const int e = tid + kThreads * i;
     if (e >= E) continue;
     int32_t run = sb[i];
     for (int v = 0; v < kRankWaves; ++v) {
