@@ -1084,8 +1084,10 @@ inline int cu_count() {
 }
 
 // Tile list of the groups of `device` (all devices with -1), in the order
-// the GEMM hands tiles out; *n_tiles receives the entry count.
-hipError_t launch_tile_table(const int32_t *groups, const int32_t *group_begin, int32_t device,
-                             int32_t P, int4 *tiles, int32_t *n_tiles, hipStream_t stream);
+// the GEMM hands tiles out; *n_tiles receives the entry count. cap: rows of
+// the group table (2E + P), all of which may be read.
+hipError_t launch_tile_table(const int32_t *groups, const int32_t *group_begin, int32_t cap,
+                             int32_t device, int32_t P, int4 *tiles, int32_t *n_tiles,
+                             hipStream_t stream);
 
 }  // namespace llep

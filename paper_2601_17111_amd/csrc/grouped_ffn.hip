@@ -53,59 +53,78 @@ size_t ffn_workspace_bytes(int64_t R, int32_t E, int32_t P, int32_t F, llep_dtyp
 // captured in a graph.
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void tile_table_kernel(const int32_t *__restrict__ groups,
-                                                         const int32_t *__restrict__ group_begin,
-                                                         int32_t device, int32_t P, int32_t BM,
-                                                         int4 *__restrict__ tiles,
-                                                         int32_t *__restrict__ n_tiles,
-                                                         int32_t *__restrict__ seq,
-                                                         int32_t *__restrict__ done) {
-  __shared__ int32_t part[256], prow[256];
-  __shared__ int32_t run, prun;
+// Thread t holds the entries 5t .. 5t+4 of the group table (up to its
+// capacity of at most kMaxChunks groups); their row counts are requested
+// together with the range's bounds (no load waits for another), and the
+// tile and padded-row bases are one exclusive scan: per thread, then over
+// the wave's lanes, then over the four waves.
+constexpr int kTileTableThreads = 256;
+constexpr int kTileTablePer = (kMaxChunks + kTileTableThreads - 1) / kTileTableThreads;
+
+__global__ __launch_bounds__(kTileTableThreads) void tile_table_kernel(
+    const int32_t *__restrict__ groups, const int32_t *__restrict__ group_begin, int32_t cap,
+    int32_t device, int32_t P, int32_t BM, int4 *__restrict__ tiles, int32_t *__restrict__ n_tiles,
+    int32_t *__restrict__ seq, int32_t *__restrict__ done) {
+  __shared__ int32_t wsum[kTileTableThreads / kWave][2];
   const int tid = threadIdx.x;
+  const int lane = tid % kWave, wave = tid / kWave;
   const int lo = device < 0 ? group_begin[0] : group_begin[device];
   const int hi = device < 0 ? group_begin[P] : group_begin[device + 1];
-  if (tid == 0) {
-    run = 0;
-    prun = 0;
+  int32_t n[kTileTablePer];
+#pragma unroll
+  for (int j = 0; j < kTileTablePer; ++j)
+    n[j] = groups[4 * min(kTileTablePer * tid + j, cap - 1) + 3];
+  int32_t mt[kTileTablePer], pr[kTileTablePer];
+  int32_t smt = 0, spr = 0;
+#pragma unroll
+  for (int j = 0; j < kTileTablePer; ++j) {
+    const int g = kTileTablePer * tid + j;
+    const bool in = g >= lo && g < hi && g < cap;
+    mt[j] = in ? (n[j] + BM - 1) / BM : 0;
+    pr[j] = in ? (n[j] + 15) / 16 * 16 : 0;
+    smt += mt[j];
+    spr += pr[j];
+  }
+  // inclusive scan over the wave, then the waves' totals
+  int32_t imt = smt, ipr = spr;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int32_t a = __shfl_up(imt, off), b = __shfl_up(ipr, off);
+    if (lane >= off) {
+      imt += a;
+      ipr += b;
+    }
+  }
+  if (lane == kWave - 1) {
+    wsum[wave][0] = imt;
+    wsum[wave][1] = ipr;
   }
   __syncthreads();
-  for (int g0 = lo; g0 < hi; g0 += 256) {
-    const int g = g0 + tid;
-    const int n = g < hi ? groups[4 * g + 3] : 0;
-    const int mt = (n + BM - 1) / BM;
-    const int pr = (n + 15) / 16 * 16;
-    part[tid] = mt;
-    prow[tid] = pr;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-      const int32_t t = tid >= off ? part[tid - off] : 0;
-      const int32_t u = tid >= off ? prow[tid - off] : 0;
-      __syncthreads();
-      part[tid] += t;
-      prow[tid] += u;
-      __syncthreads();
+  int32_t base = imt - smt, pbase = ipr - spr, total = 0;
+  for (int w = 0; w < kTileTableThreads / kWave; ++w) {
+    if (w < wave) {
+      base += wsum[w][0];
+      pbase += wsum[w][1];
     }
-    const int32_t base = run + part[tid] - mt;
-    const int32_t pbase = prun + prow[tid] - pr;
-    for (int i = 0; i < mt; ++i) tiles[base + i] = make_int4(g, i, pbase, 0);
-    __syncthreads();
-    if (tid == 255) {
-      run += part[255];
-      prun += prow[255];
-    }
-    __syncthreads();
+    total += wsum[w][0];
   }
-  if (tid == 0) *n_tiles = run;
+#pragma unroll
+  for (int j = 0; j < kTileTablePer; ++j) {
+    const int g = kTileTablePer * tid + j;
+    for (int i = 0; i < mt[j]; ++i) tiles[base + i] = make_int4(g, i, pbase, 0);
+    base += mt[j];
+    pbase += pr[j];
+  }
+  if (tid == 0) *n_tiles = total;
   if (seq != nullptr && tid < 16) seq[tid] = 0;
   if (done != nullptr)
-    for (int i = tid; i < run; i += 256) done[i] = 0;
+    for (int i = tid; i < total; i += kTileTableThreads) done[i] = 0;
 }
 
-hipError_t launch_tile_table(const int32_t *groups, const int32_t *group_begin, int32_t device,
-                             int32_t P, int4 *tiles, int32_t *n_tiles, hipStream_t stream) {
-  hipLaunchKernelGGL(tile_table_kernel, dim3(1), dim3(256), 0, stream, groups, group_begin,
-                     device, P, kTileM, tiles, n_tiles, nullptr, nullptr);
+hipError_t launch_tile_table(const int32_t *groups, const int32_t *group_begin, int32_t cap,
+                             int32_t device, int32_t P, int4 *tiles, int32_t *n_tiles,
+                             hipStream_t stream) {
+  hipLaunchKernelGGL(tile_table_kernel, dim3(1), dim3(kTileTableThreads), 0, stream, groups,
+                     group_begin, cap, device, P, kTileM, tiles, n_tiles, nullptr, nullptr);
   return hipGetLastError();
 }
 
@@ -483,8 +502,9 @@ hipError_t launch_grouped_ffn(const FfnArgs &a, hipStream_t stream) {
   void *act = ws + L.act_off;
   if (a.dtype == LLEP_BF16) {
     const int grid = (cu_count() + 7) / 8 * 8;  // one workgroup per CU, XCD-balanced
-    hipLaunchKernelGGL(tile_table_kernel, dim3(1), dim3(256), 0, stream, a.groups, a.group_begin,
-                       a.device, a.P, kTileM, tiles, n_mtiles, seq, done);
+    hipLaunchKernelGGL(tile_table_kernel, dim3(1), dim3(kTileTableThreads), 0, stream, a.groups,
+                       a.group_begin, 2 * a.E + a.P, a.device, a.P, kTileM, tiles, n_mtiles, seq,
+                       done);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmArgs g1 = {};

@@ -477,7 +477,8 @@ hipError_t launch_grouped_ffn_backward(const FfnBwdArgs &a, hipStream_t stream) 
     err = hipGetLastError();           \
     if (err != hipSuccess) return err; \
   } while (0)
-  err = launch_tile_table(a.groups, a.group_begin, a.device, a.P, tiles, n_mtiles, stream);
+  err = launch_tile_table(a.groups, a.group_begin, 2 * a.E + a.P, a.device, a.P, tiles, n_mtiles,
+                          stream);
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(wgrad_table_kernel, dim3(1), dim3(1024), 0, stream, a.groups, a.group_begin,
                      a.device, a.P, a.E, a.E / a.P, kbase, chunk, wge, n_wg, 2 * F / kSK,
