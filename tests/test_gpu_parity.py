@@ -121,6 +121,39 @@ def test_plan_tight_capacity_matches_oracle(dev, case):
     assert_plan_equal(got, info, ref)
 
 
+def _repeated_chunk_cases():
+    """Plans in which one expert has two or more chunks on the same device
+    (an over-tight capacity sends force-assigned remainders back to devices
+    that already hold a chunk of the expert): the table layout then has to
+    merge chunks into one group and order them by start within it."""
+    rng = np.random.default_rng(4242)
+    cases = []
+    while len(cases) < 12:
+        P = int(rng.choice([2, 3, 4, 8]))
+        M = int(rng.integers(1, 5))
+        E = P * M
+        T, K = int(rng.integers(200, 2500)), int(rng.integers(1, 4))
+        hot = rng.choice(E, size=max(1, E // 4), replace=False)
+        ids = np.where(rng.random((T, K)) < 0.7, rng.choice(hot, size=(T, K)),
+                       rng.integers(0, E, (T, K))).astype(np.int32)
+        cap = max(1, int(math.ceil(T * K / P) * float(rng.choice([0.3, 0.5]))))
+        m = int(rng.choice([3, 50]))
+        ref = oracle.plan(ids.reshape(-1).tolist(), E, P, cap, m)
+        if len(ref.chunks) > len(ref.groups):
+            cases.append((ids, E, P, cap, m))
+    return cases
+
+
+@pytest.mark.parametrize("case", _repeated_chunk_cases(),
+                         ids=lambda c: f"E{c[1]}P{c[2]}R{c[0].size}cap{c[3]}m{c[4]}")
+def test_plan_repeated_device_chunks_matches_oracle(dev, case):
+    ids, E, P, cap, m = case
+    got, info, _ = run_plan(ids, E, P, cap, m, dev=dev)
+    ref = oracle.plan(ids.reshape(-1).tolist(), E, P, cap, m)
+    assert len(ref.chunks) > len(ref.groups)
+    assert_plan_equal(got, info, ref)
+
+
 @pytest.mark.parametrize("E,P", [(512, 64), (512, 8), (256, 64)])
 def test_plan_max_sizes(dev, E, P):
     rng = np.random.default_rng(E + P)
