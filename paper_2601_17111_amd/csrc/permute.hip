@@ -163,6 +163,9 @@ __global__ __launch_bounds__(256) void rank_kernel(
 // piece of a row, so each wave issues K stores) beats a wave per whole row
 // (6 vectors per lane, 6 K stores): 2-6% on the gpt-oss shapes, 5% on
 // deepseek-v3, 0.5% on qwen3; 2 or 3 vectors per lane fall in between.
+// Workgroups of 2 waves (grid capped at 65536, so on the larger shapes a
+// wave takes a second piece) beat 4 waves by 1.3-3.4%; 8 waves, 1 wave,
+// an uncapped grid and caps of 16384 or 32768 were slower or mixed.
 // Four pairs' rows of at most 4 vectors per lane are in flight per combine
 // step (1 or 2 pairs measured within 2%; 1 or 2 vectors per lane, a wave
 // per 1 or 2 KB of the output row, within 1%: the combine's stream is
@@ -205,8 +208,14 @@ inline int vecs_per_lane(int32_t vecs, int max_per_lane) {
 // with kV = 1): the slice is loaded once (all kV vectors per lane in flight)
 // and stored to the rows of the token's K pairs. Row indices come in as one vector load per 64 pairs and are read
 // back with v_readlane, so the stores need no further memory round trip.
+// Workgroups of kGatherWaves waves, at most kGatherGrid of them (each wave
+// then takes a second item when there are more than kGatherGrid workgroups'
+// worth of items).
+constexpr int kGatherWaves = 2;
+constexpr int kGatherGrid = 65536;
+
 template <int kV>
-__global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x,
+__global__ __launch_bounds__(kGatherWaves * kWave) void gather_kernel(const i32x4 *__restrict__ x,
                                                      i32x4 *__restrict__ x_perm,
                                                      const int32_t *__restrict__ pair_row,
                                                      int64_t T, int32_t K, int32_t vecs,
@@ -214,8 +223,8 @@ __global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = lane_id();
   const int nslices = (vecs + kV * kWave - 1) / (kV * kWave);
-  for (int64_t wid = int64_t(blockIdx.x) * 4 + w; wid < T * nslices;
-       wid += int64_t(gridDim.x) * 4) {
+  for (int64_t wid = int64_t(blockIdx.x) * kGatherWaves + w; wid < T * nslices;
+       wid += int64_t(gridDim.x) * kGatherWaves) {
     const int64_t t = wid / nslices;
     const i32x4 *src = x + t * vecs;
     {
@@ -246,7 +255,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const i32x4 *__restrict__ x
 
 template <int kV>
 void launch_gather_v(int grid, hipStream_t stream, const PermuteArgs &a, int32_t vecs) {
-  hipLaunchKernelGGL(gather_kernel<kV>, dim3(grid), dim3(256), 0, stream,
+  hipLaunchKernelGGL(gather_kernel<kV>, dim3(grid), dim3(kGatherWaves * kWave), 0, stream,
                      static_cast<const i32x4 *>(a.x), static_cast<i32x4 *>(a.x_perm),
                      a.pair_row, a.T, a.K, vecs, a.R);
 }
@@ -262,8 +271,8 @@ hipError_t launch_permute(const PermuteArgs &a, hipStream_t stream) {
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int32_t vecs = int32_t((int64_t(a.D) * a.elem_bytes) / 16);
-  const int64_t blocks = (a.T * ((vecs + kWave - 1) / kWave) + 3) / 4;
-  const int grid = int(blocks < 65536 ? blocks : 65536);
+  const int64_t blocks = (a.T * ((vecs + kWave - 1) / kWave) + kGatherWaves - 1) / kGatherWaves;
+  const int grid = int(blocks < kGatherGrid ? blocks : kGatherGrid);
   launch_gather_v<1>(grid, stream, a, vecs);
   return hipGetLastError();
 }
